@@ -1,0 +1,157 @@
+/*
+ * lumen_kv_ckpt: paged KV-cache checkpoint and restore data movement on
+ * MI355X (gfx950).
+ *
+ * LUMEN keeps a checkpoint of every in-flight request's KV cache so that a
+ * request interrupted by a worker failure resumes from its checkpointed
+ * prefix instead of re-running prefill (Sec. 4.2, load-aware KV
+ * checkpointing; Sec. 4.3, KV-reuse recovery).  This library moves the bytes
+ * of that scheme on one GPU:
+ *
+ *   plan    device prefix sum that assigns checkpoint rows to each request's
+ *           token range [start, end)  (the newly written tokens, Sec. 4.2)
+ *   pack    gather of those tokens out of the paged cache through each
+ *           request's block table into contiguous token-major rows
+ *           (the copy of new KV pages out of GPU memory, Sec. 4.2 step 3)
+ *   unpack  scatter of checkpoint rows into the blocks a new block table
+ *           names (loading the checkpointed pages back into GPU memory,
+ *           Sec. 4.3)
+ *   offload / stage_in
+ *           device->pinned-host and pinned-host->device copies of packed
+ *           rows on a side stream, ordered after (before) the main stream's
+ *           work (the pinned CPU buffer of Sec. 4.2)
+ *
+ * Layouts.  The cache is one allocation of 16-bit elements (bf16, moved as
+ * raw bits), layer-major, K before V:
+ *   LUMEN_CACHE_NHD  [L][2][num_blocks][block_size][H][D]
+ *   LUMEN_CACHE_HND  [L][2][num_blocks][H][block_size][D]
+ * A block (page) holds block_size consecutive token positions of one request
+ * (Sec. 2.1).  Block table row r, of bt_cols int32 entries, maps request r's
+ * page j (tokens [j*block_size, (j+1)*block_size)) to a physical block.
+ * A checkpoint row holds one token, all layers, K and V, token-major:
+ *   row [L][2][H][D]   (row_bytes = L*2*H*D*2)
+ * so the rows of successive increments append to a request's checkpoint and
+ * any prefix of rows is a token prefix (the longest checkpointed prefix that
+ * recovery restores, Sec. 4.3).
+ *
+ * Ownership and ordering.  Every buffer is allocated and owned by the
+ * caller; the library allocates no device memory.  All calls are
+ * asynchronous and stream-ordered on the hipStream_t passed as `stream`
+ * (NULL is the null stream), except lumen_kv_ckpt_status, which
+ * synchronises that stream.  A workspace must not be shared by calls that
+ * are in flight at the same time.
+ *
+ * Errors.  Argument errors the host can see are returned synchronously
+ * (negative codes) and nothing is enqueued.  Errors that depend on device
+ * data (ranges, block ids, capacity) are recorded in the workspace's error
+ * word: the offending token rows are skipped, all other rows are still
+ * copied, and the word keeps the most negative code seen.  lumen_kv_ckpt_plan
+ * starts a new error epoch (it overwrites the word with its own result);
+ * lumen_kv_ckpt_status reads and clears it.
+ */
+#ifndef LUMEN_KV_CKPT_H
+#define LUMEN_KV_CKPT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LUMEN_OK 0
+#define LUMEN_ERR_INVALID_ARG (-1) /* null pointer, negative size, bad dims */
+#define LUMEN_ERR_UNSUPPORTED (-2) /* elem_bytes != 2, unknown order, D*2 % 16 */
+#define LUMEN_ERR_MISALIGNED (-3)  /* cache/ckpt/workspace not 16-byte aligned */
+#define LUMEN_ERR_HIP (-4)         /* a HIP runtime call failed */
+#define LUMEN_ERR_RANGE (-5)       /* start < 0, end < start, or a page past bt_cols */
+#define LUMEN_ERR_BLOCK_ID (-6)    /* block table entry outside [0, num_blocks) */
+#define LUMEN_ERR_CAPACITY (-7)    /* checkpoint row outside [0, ckpt_rows) */
+
+#define LUMEN_CACHE_NHD 0
+#define LUMEN_CACHE_HND 1
+
+/* A hipStream_t, passed as an opaque pointer so that this header does not
+ * depend on the HIP headers. */
+typedef void *lumen_stream_t;
+
+typedef struct lumen_kv_layout {
+    int32_t num_layers;   /* L */
+    int32_t num_kv_heads; /* H: KV heads held by this GPU */
+    int32_t head_dim;     /* D; D*elem_bytes must be a multiple of 16 */
+    int32_t block_size;   /* tokens per block (page) */
+    int64_t num_blocks;   /* blocks in the pool */
+    int32_t elem_bytes;   /* must be 2 (bf16/fp16, copied as raw bits) */
+    int32_t cache_order;  /* LUMEN_CACHE_NHD or LUMEN_CACHE_HND */
+} lumen_kv_layout;
+
+/* Bytes of device workspace a plan over num_reqs requests needs (header,
+ * per-request row offsets and starts).  Returns 0 if num_reqs < 0. */
+size_t lumen_kv_ckpt_plan_workspace_bytes(int32_t num_reqs);
+
+/* Row plan for one set of token ranges (Sec. 4.2: only tokens written since
+ * the last checkpoint are sent).  Device inputs d_start[num_reqs],
+ * d_end[num_reqs] (int32).  Request r contributes n_r = end-start rows.
+ * Rows are packed (d_req_row_base == NULL): request r's first row is
+ * row_base + sum_{r'<r} n_r', in request order; or per-request
+ * (d_req_row_base = device int64[num_reqs]): token t of request r goes to
+ * row d_req_row_base[r] + t, so each request appends to its own reserved
+ * checkpoint region.  A request with start < 0 or end < start contributes
+ * no rows and records LUMEN_ERR_RANGE.  One plan serves any number of pack
+ * and unpack calls over the same ranges.  d_workspace: device memory of
+ * lumen_kv_ckpt_plan_workspace_bytes(num_reqs) bytes, 16-byte aligned. */
+int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
+                       int32_t num_reqs, int64_t row_base,
+                       const int64_t *d_req_row_base, void *d_workspace,
+                       lumen_stream_t stream);
+
+/* Checkpoint gather (Sec. 4.2, copy of new KV pages out of GPU memory): for
+ * every request r of the plan and token t in [start_r, end_r), copies the
+ * token's K and V of every layer from block d_block_tables[r*bt_cols +
+ * t/block_size], slot t % block_size, of d_cache into checkpoint row
+ * row(r, t) of d_ckpt, which has room for ckpt_rows rows.  Per token row,
+ * checked in this order: page t/block_size < bt_cols (RANGE); block id in
+ * [0, num_blocks) (BLOCK_ID); row in [0, ckpt_rows) (CAPACITY).  num_reqs
+ * must equal the plan's.  d_cache and d_ckpt 16-byte aligned; a buffer may
+ * be NULL only if it is empty (num_blocks, ckpt_rows or bt_cols is 0). */
+int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
+                       const int32_t *d_block_tables, int32_t bt_cols,
+                       int32_t num_reqs, void *d_workspace, void *d_ckpt,
+                       int64_t ckpt_rows, lumen_stream_t stream);
+
+/* Restore scatter (Sec. 4.3, loading checkpointed pages into GPU memory):
+ * the inverse of lumen_kv_ckpt_pack under d_block_tables (usually freshly
+ * allocated, fragmented blocks).  Writes only the slots of the planned
+ * tokens; every other byte of d_cache is left untouched.  Two planned tokens
+ * mapping to the same (block, slot) race; the allocator must not do that. */
+int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
+                         const int32_t *d_block_tables, int32_t bt_cols,
+                         int32_t num_reqs, void *d_workspace,
+                         const void *d_ckpt, int64_t ckpt_rows,
+                         lumen_stream_t stream);
+
+/* Synchronises `stream`, then returns and clears the workspace's error word
+ * (LUMEN_OK if no device-side error was recorded since the last plan). */
+int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream);
+
+/* Static string for a status code. */
+const char *lumen_kv_ckpt_strerror(int code);
+
+/* Device -> host copy of `bytes` from d_src to h_dst on stream `side`,
+ * ordered after all work enqueued on `producer` so far, so the main stream
+ * goes on without waiting (Sec. 4.2: the background copy of new pages to a
+ * pinned CPU buffer).  h_dst should be pinned (hipHostMalloc) for the copy
+ * to overlap. The caller synchronises `side` before reading h_dst. */
+int lumen_kv_ckpt_offload(const void *d_src, void *h_dst, size_t bytes,
+                          lumen_stream_t producer, lumen_stream_t side);
+
+/* Host -> device copy of `bytes` from h_src to d_dst on stream `side`; work
+ * enqueued on `consumer` afterwards waits for it (restore from a host
+ * checkpoint store, Sec. 4.3). */
+int lumen_kv_ckpt_stage_in(const void *h_src, void *d_dst, size_t bytes,
+                           lumen_stream_t side, lumen_stream_t consumer);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LUMEN_KV_CKPT_H */

@@ -1,0 +1,567 @@
+// Paged KV-cache checkpoint pack / restore unpack for MI355X (gfx950).
+//
+// The operations and layouts are specified in include/lumen_kv_ckpt.h.  This
+// file holds the three kernels (row plan, gather, scatter) and the C ABI.
+//
+// Work decomposition.  A checkpoint is a sequence of token rows, each
+// [L][2][H][D] 16-bit elements.  The copy is split into units of
+// (token row, layer): one unit is the K and V of one token in one layer,
+// 2*H*D*2 bytes, contiguous on the checkpoint side.  Units are numbered in
+// checkpoint order, u = packed_row * L + layer, and a persistent grid of
+// wavefronts splits [0, total_units) into equal contiguous spans, so every
+// wavefront moves the same number of bytes whatever the mix of request
+// lengths.  Inside its span a wavefront walks token rows in order: the
+// request, its block-table entry and the checkpoint row of each token are
+// wave-uniform and live in scalar registers; the 64 lanes then move the
+// token's units as 16-byte vectors.  On the checkpoint side those vectors
+// are one contiguous run; on the cache side they are runs of H*D*2 bytes
+// (token-major cache) or D*2 bytes (head-major cache), each a whole number
+// of 128-byte lines for the serving shapes, so every access is full-line and
+// no LDS staging is needed for the head-major transpose.
+
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <stdlib.h>
+
+#include <mutex>
+
+#include "lumen_kv_ckpt.h"
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kBlockThreads = 256;
+constexpr int kWavesPerBlock = kBlockThreads / kWave;
+constexpr int kPlanThreads = 1024;
+constexpr int kUnroll = 8;  // 16-byte vectors in flight per lane
+constexpr int kDefaultWavesPerCU = 16;
+
+// Workspace layout (device memory, caller-owned):
+//   WsHeader, then int64 prefix[R+1], int64 first_row[R], int32 start[R].
+struct WsHeader {
+  int64_t total_rows;  // sum of the valid requests' token counts
+  int32_t num_reqs;
+  int32_t err;  // most negative device-side status since the plan
+  int64_t reserved[6];
+};
+static_assert(sizeof(WsHeader) == 64, "header size");
+
+constexpr size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
+
+struct WsView {
+  WsHeader *hdr;
+  int64_t *prefix;
+  int64_t *first_row;
+  int32_t *start;
+};
+
+WsView ws_view(void *ws, int32_t R) {
+  char *p = static_cast<char *>(ws);
+  WsView v;
+  v.hdr = reinterpret_cast<WsHeader *>(p);
+  size_t off = sizeof(WsHeader);
+  v.prefix = reinterpret_cast<int64_t *>(p + off);
+  off = align16(off + sizeof(int64_t) * (size_t(R) + 1));
+  v.first_row = reinterpret_cast<int64_t *>(p + off);
+  off = align16(off + sizeof(int64_t) * size_t(R));
+  v.start = reinterpret_cast<int32_t *>(p + off);
+  return v;
+}
+
+size_t ws_bytes(int32_t R) {
+  size_t off = sizeof(WsHeader);
+  off = align16(off + sizeof(int64_t) * (size_t(R) + 1));
+  off = align16(off + sizeof(int64_t) * size_t(R));
+  off = align16(off + sizeof(int32_t) * size_t(R));
+  return off;
+}
+
+// Division by a run-time constant d >= 1 with a multiply-high, valid for
+// dividends below 2^31 (round-up reciprocal of Granlund and Montgomery,
+// "Division by invariant integers using multiplication", PLDI 1994).
+struct FastDiv {
+  uint32_t d, mul, shift;
+};
+
+FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((uint64_t(1) << l) < d) ++l;
+  FastDiv f;
+  f.d = d;
+  f.shift = l;
+  f.mul = uint32_t(((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1);
+  return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
+  return (__umulhi(n, f.mul) + n) >> f.shift;
+}
+
+// Geometry shared by the gather and the scatter.
+struct Geom {
+  int64_t slab_bytes;   // stride of one (layer, K/V) slab: NB*bs*H*D*2
+  int64_t block_bytes;  // stride of one block inside a slab: bs*H*D*2
+  int64_t row_bytes;    // one checkpoint row: L*2*H*D*2
+  int64_t num_blocks;
+  int64_t ckpt_rows;
+  int32_t num_layers;
+  int32_t block_size;
+  int32_t slot_bytes;   // stride of one slot: H*D*2 (NHD) or D*2 (HND)
+  int32_t head_bytes;   // HND: stride of one head, bs*D*2
+  int32_t unit_vecs;    // 16-byte vectors per (token, layer): 2*H*D*2/16
+  int32_t bt_cols;
+  int32_t num_reqs;
+  FastDiv div_unit;     // by unit_vecs
+  FastDiv div_kv;       // by H*D*2/16, vectors of one (token, layer, K/V)
+  FastDiv div_head;     // by D*2/16, vectors of one head
+  FastDiv div_bs;       // by block_size
+};
+
+__device__ __forceinline__ void record_error(int32_t *err, int code) {
+  if ((threadIdx.x & (kWave - 1)) == 0) atomicMin(err, code);
+}
+
+// Byte offset, relative to (block, slot) of layer 0 / K, of vector `vv` of a
+// token's checkpoint row segment (vv counts 16-byte vectors from the start of
+// the row: layer-major, then K/V, then head, then dim).
+template <bool kHeadMajor>
+__device__ __forceinline__ int64_t cache_vec_offset(uint32_t vv,
+                                                    const Geom &g) {
+  const uint32_t l = fdiv(vv, g.div_unit);
+  const uint32_t w = vv - l * uint32_t(g.unit_vecs);
+  const uint32_t kv = fdiv(w, g.div_kv);
+  const uint32_t x = w - kv * g.div_kv.d;
+  int64_t off = int64_t(l * 2 + kv) * g.slab_bytes;
+  if (kHeadMajor) {
+    const uint32_t h = fdiv(x, g.div_head);
+    const uint32_t y = x - h * g.div_head.d;
+    off += int64_t(h) * g.head_bytes + int64_t(y) * 16;
+  } else {
+    off += int64_t(x) * 16;
+  }
+  return off;
+}
+
+// One batch of kUnroll vectors per lane: all loads first, then all stores,
+// so each lane keeps kUnroll 16-byte requests in flight.  kPred guards the
+// last, partial batch of a row segment.
+template <bool kPack, bool kHeadMajor, bool kPred>
+__device__ __forceinline__ void copy_batch(const uint8_t *__restrict__ src,
+                                           uint8_t *__restrict__ dst,
+                                           int64_t cache_tok, int64_t ckpt_off,
+                                           uint32_t vbase, int32_t v0,
+                                           int32_t nvec, int lane,
+                                           const Geom &g) {
+  uint4 buf[kUnroll];
+#pragma unroll
+  for (int k = 0; k < kUnroll; ++k) {
+    const int32_t v = v0 + k * kWave + lane;
+    buf[k] = make_uint4(0, 0, 0, 0);
+    if (!kPred || v < nvec) {
+      const int64_t off =
+          kPack ? cache_tok + cache_vec_offset<kHeadMajor>(vbase + v, g)
+                : ckpt_off + int64_t(v) * 16;
+      buf[k] = *reinterpret_cast<const uint4 *>(src + off);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kUnroll; ++k) {
+    const int32_t v = v0 + k * kWave + lane;
+    if (!kPred || v < nvec) {
+      const int64_t off =
+          kPack ? ckpt_off + int64_t(v) * 16
+                : cache_tok + cache_vec_offset<kHeadMajor>(vbase + v, g);
+      *reinterpret_cast<uint4 *>(dst + off) = buf[k];
+    }
+  }
+}
+
+// One persistent kernel for both directions.  kPack: cache -> checkpoint;
+// otherwise checkpoint -> cache.
+template <bool kPack, bool kHeadMajor>
+__global__ __launch_bounds__(kBlockThreads) void copy_rows_kernel(
+    const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
+    const int32_t *__restrict__ block_tables,
+    const WsHeader *__restrict__ hdr, const int64_t *__restrict__ prefix,
+    const int64_t *__restrict__ first_row, const int32_t *__restrict__ start,
+    int32_t *err, Geom g) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wave;
+  const int64_t nw = int64_t(gridDim.x) * kWavesPerBlock;
+
+  if (hdr->num_reqs != g.num_reqs) {
+    if (gw == 0) record_error(err, LUMEN_ERR_INVALID_ARG);
+    return;
+  }
+  const int64_t L = g.num_layers;
+  const int64_t units = hdr->total_rows * L;
+  int64_t u = units * gw / nw;
+  const int64_t u_end = units * (gw + 1) / nw;
+  if (u >= u_end) return;
+
+  // First token row of the span and the request that owns it: the last
+  // request whose prefix does not exceed the row (empty requests share
+  // their successor's prefix and are skipped by taking the last).
+  int64_t row = u / L;
+  int32_t l0 = int32_t(u - row * L);
+  int32_t lo = 0, hi = g.num_reqs - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (prefix[mid] <= row) lo = mid; else hi = mid - 1;
+  }
+  int32_t r = lo;
+  int64_t row_end = prefix[r + 1];
+  int64_t t = start[r] + (row - prefix[r]);
+  int64_t crow = first_row[r] + (row - prefix[r]);
+
+  while (true) {
+    const int32_t nl = int32_t(min(int64_t(g.num_layers - l0), u_end - u));
+    const uint32_t page = fdiv(uint32_t(t), g.div_bs);
+    const uint32_t slot = uint32_t(t) - page * uint32_t(g.block_size);
+    int code = LUMEN_OK;
+    int64_t b = -1;
+    if (page >= uint32_t(g.bt_cols)) {
+      code = LUMEN_ERR_RANGE;
+    } else {
+      b = block_tables[int64_t(r) * g.bt_cols + page];
+      if (b < 0 || b >= g.num_blocks)
+        code = LUMEN_ERR_BLOCK_ID;
+      else if (crow < 0 || crow >= g.ckpt_rows)
+        code = LUMEN_ERR_CAPACITY;
+    }
+    if (code != LUMEN_OK) {
+      record_error(err, code);
+    } else {
+      // Cache side: (block, slot) of layer 0 / K; checkpoint side: the
+      // span's first unit in this row.
+      const int64_t cache_tok = b * g.block_bytes + int64_t(slot) * g.slot_bytes;
+      const int64_t ckpt_off =
+          crow * g.row_bytes + int64_t(l0) * g.unit_vecs * 16;
+      const uint32_t vbase = uint32_t(l0) * uint32_t(g.unit_vecs);
+      const int32_t nvec = nl * g.unit_vecs;
+      constexpr int32_t kBatch = kWave * kUnroll;
+      int32_t v0 = 0;
+      for (; v0 + kBatch <= nvec; v0 += kBatch)
+        copy_batch<kPack, kHeadMajor, false>(src, dst, cache_tok, ckpt_off,
+                                             vbase, v0, nvec, lane, g);
+      if (v0 < nvec)
+        copy_batch<kPack, kHeadMajor, true>(src, dst, cache_tok, ckpt_off,
+                                            vbase, v0, nvec, lane, g);
+    }
+    u += nl;
+    if (u >= u_end) break;
+    l0 = 0;
+    ++row;
+    ++t;
+    ++crow;
+    if (row == row_end) {
+      // Next request with rows; one exists because row < total_rows.
+      do {
+        ++r;
+      } while (prefix[r + 1] == row);
+      row_end = prefix[r + 1];
+      t = start[r];
+      crow = first_row[r];
+    }
+  }
+}
+
+// Row plan: one workgroup scans the per-request token counts.
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(
+    const int32_t *__restrict__ d_start, const int32_t *__restrict__ d_end,
+    int32_t R, int64_t row_base, const int64_t *__restrict__ req_row_base,
+    WsHeader *hdr, int64_t *prefix, int64_t *first_row, int32_t *start) {
+  __shared__ int64_t scan[kPlanThreads];
+  __shared__ int bad;
+  const int tid = threadIdx.x;
+  if (tid == 0) bad = 0;
+  const int32_t per = (R + kPlanThreads - 1) / kPlanThreads;
+  const int32_t lo = min(R, tid * per);
+  const int32_t hi = min(R, lo + per);
+  int64_t local = 0;
+  int my_bad = 0;
+  for (int32_t i = lo; i < hi; ++i) {
+    const int32_t s = d_start[i], e = d_end[i];
+    if (s < 0 || e < s) my_bad = 1; else local += int64_t(e) - s;
+  }
+  scan[tid] = local;
+  __syncthreads();
+  if (my_bad) atomicOr(&bad, 1);
+  // Inclusive Hillis-Steele scan of the per-thread sums.
+  for (int off = 1; off < kPlanThreads; off <<= 1) {
+    const int64_t add = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += add;
+    __syncthreads();
+  }
+  int64_t run = scan[tid] - local;  // exclusive
+  for (int32_t i = lo; i < hi; ++i) {
+    const int32_t s = d_start[i], e = d_end[i];
+    const bool ok = !(s < 0 || e < s);
+    const int64_t n = ok ? int64_t(e) - s : 0;
+    prefix[i] = run;
+    first_row[i] = req_row_base ? req_row_base[i] + s : row_base + run;
+    start[i] = ok ? s : 0;
+    run += n;
+  }
+  if (tid == kPlanThreads - 1) {
+    prefix[R] = scan[tid];
+    hdr->total_rows = scan[tid];
+    hdr->num_reqs = R;
+  }
+  __syncthreads();
+  if (tid == 0) hdr->err = bad ? LUMEN_ERR_RANGE : LUMEN_OK;
+}
+
+// ------------------------------------------------------------- host side
+
+constexpr int kMaxDevices = 64;
+
+struct DeviceInfo {
+  std::once_flag once;
+  int cus = 0;
+  hipEvent_t order_event = nullptr;
+  std::mutex event_mu;
+};
+DeviceInfo g_dev[kMaxDevices];
+
+int waves_per_cu() {
+  static int w = [] {
+    const char *e = getenv("LUMEN_KV_CKPT_WAVES_PER_CU");
+    int v = e ? atoi(e) : kDefaultWavesPerCU;
+    return v > 0 && v <= 64 ? v : kDefaultWavesPerCU;
+  }();
+  return w;
+}
+
+int current_device(DeviceInfo **info) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return LUMEN_ERR_HIP;
+  DeviceInfo &d = g_dev[dev];
+  std::call_once(d.once, [&] {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount,
+                              dev) == hipSuccess)
+      d.cus = cus;
+    hipEvent_t ev = nullptr;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess)
+      d.order_event = ev;
+  });
+  if (d.cus <= 0 || !d.order_event) return LUMEN_ERR_HIP;
+  *info = &d;
+  return LUMEN_OK;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_layout(const lumen_kv_layout *lay) {
+  if (!lay) return LUMEN_ERR_INVALID_ARG;
+  if (lay->num_layers <= 0 || lay->num_kv_heads <= 0 || lay->head_dim <= 0 ||
+      lay->block_size <= 0 || lay->num_blocks < 0)
+    return LUMEN_ERR_INVALID_ARG;
+  if (lay->elem_bytes != 2) return LUMEN_ERR_UNSUPPORTED;
+  if (lay->cache_order != LUMEN_CACHE_NHD && lay->cache_order != LUMEN_CACHE_HND)
+    return LUMEN_ERR_UNSUPPORTED;
+  if ((int64_t(lay->head_dim) * lay->elem_bytes) % 16 != 0)
+    return LUMEN_ERR_UNSUPPORTED;
+  // Vector indices within a row and token positions are 32-bit.
+  const int64_t row_bytes = int64_t(lay->num_layers) * 2 * lay->num_kv_heads *
+                            lay->head_dim * lay->elem_bytes;
+  if (row_bytes / 16 >= (int64_t(1) << 31)) return LUMEN_ERR_UNSUPPORTED;
+  return LUMEN_OK;
+}
+
+int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
+                void *dst, const int32_t *bt, int32_t bt_cols,
+                int32_t num_reqs, void *ws, int64_t ckpt_rows,
+                lumen_stream_t stream) {
+  int st = check_layout(lay);
+  if (st != LUMEN_OK) return st;
+  if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0) return LUMEN_ERR_INVALID_ARG;
+  if (!ws) return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(ws)) return LUMEN_ERR_MISALIGNED;
+  if (num_reqs == 0) return LUMEN_OK;
+  // A buffer may be null only when it is empty; the device checks then keep
+  // every access away from it.
+  const void *cache = pack ? src : dst;
+  const void *ckpt = pack ? dst : src;
+  if ((!cache && lay->num_blocks > 0) || (!ckpt && ckpt_rows > 0) ||
+      (!bt && bt_cols > 0))
+    return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(src) || !aligned16(dst)) return LUMEN_ERR_MISALIGNED;
+  DeviceInfo *dev = nullptr;
+  st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+
+  const int64_t H = lay->num_kv_heads, D = lay->head_dim;
+  const int64_t bs = lay->block_size;
+  const int64_t d_bytes = D * lay->elem_bytes;
+  Geom g;
+  g.block_bytes = bs * H * d_bytes;
+  g.slab_bytes = lay->num_blocks * g.block_bytes;
+  g.row_bytes = int64_t(lay->num_layers) * 2 * H * d_bytes;
+  g.num_blocks = lay->num_blocks;
+  g.ckpt_rows = ckpt_rows;
+  g.num_layers = lay->num_layers;
+  g.block_size = lay->block_size;
+  const bool hnd = lay->cache_order == LUMEN_CACHE_HND;
+  g.slot_bytes = int32_t(hnd ? d_bytes : H * d_bytes);
+  g.head_bytes = int32_t(hnd ? bs * d_bytes : 0);
+  g.unit_vecs = int32_t(2 * H * d_bytes / 16);
+  g.bt_cols = bt_cols;
+  g.num_reqs = num_reqs;
+  g.div_unit = make_fastdiv(uint32_t(g.unit_vecs));
+  g.div_kv = make_fastdiv(uint32_t(H * d_bytes / 16));
+  g.div_head = make_fastdiv(uint32_t(d_bytes / 16));
+  g.div_bs = make_fastdiv(uint32_t(bs));
+
+  WsView v = ws_view(ws, num_reqs);
+  // Persistent grid: enough waves to keep every CU's memory pipeline full,
+  // and never more waves than the checkpoint could hold units.
+  int64_t waves = int64_t(dev->cus) * waves_per_cu();
+  const int64_t max_units = ckpt_rows * int64_t(lay->num_layers);
+  if (max_units < waves) waves = max_units > 0 ? max_units : 1;
+  const unsigned blocks = unsigned((waves + kWavesPerBlock - 1) / kWavesPerBlock);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint8_t *in = static_cast<const uint8_t *>(src);
+  uint8_t *out = static_cast<uint8_t *>(dst);
+  if (pack) {
+    if (hnd)
+      hipLaunchKernelGGL((copy_rows_kernel<true, true>), dim3(blocks),
+                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
+                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+    else
+      hipLaunchKernelGGL((copy_rows_kernel<true, false>), dim3(blocks),
+                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
+                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+  } else {
+    if (hnd)
+      hipLaunchKernelGGL((copy_rows_kernel<false, true>), dim3(blocks),
+                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
+                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+    else
+      hipLaunchKernelGGL((copy_rows_kernel<false, false>), dim3(blocks),
+                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
+                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+  }
+  return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lumen_kv_ckpt_plan_workspace_bytes(int32_t num_reqs) {
+  return num_reqs < 0 ? 0 : ws_bytes(num_reqs);
+}
+
+int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
+                       int32_t num_reqs, int64_t row_base,
+                       const int64_t *d_req_row_base, void *d_workspace,
+                       lumen_stream_t stream) {
+  if (num_reqs < 0 || !d_workspace) return LUMEN_ERR_INVALID_ARG;
+  if (num_reqs > 0 && (!d_start || !d_end)) return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(d_workspace)) return LUMEN_ERR_MISALIGNED;
+  DeviceInfo *dev = nullptr;
+  int st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  WsView v = ws_view(d_workspace, num_reqs);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0,
+                     static_cast<hipStream_t>(stream), d_start, d_end,
+                     num_reqs, row_base, d_req_row_base, v.hdr, v.prefix,
+                     v.first_row, v.start);
+  return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
+}
+
+int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
+                       const int32_t *d_block_tables, int32_t bt_cols,
+                       int32_t num_reqs, void *d_workspace, void *d_ckpt,
+                       int64_t ckpt_rows, lumen_stream_t stream) {
+  return launch_copy(true, layout, d_cache, d_ckpt, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, ckpt_rows, stream);
+}
+
+int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
+                         const int32_t *d_block_tables, int32_t bt_cols,
+                         int32_t num_reqs, void *d_workspace,
+                         const void *d_ckpt, int64_t ckpt_rows,
+                         lumen_stream_t stream) {
+  return launch_copy(false, layout, d_ckpt, d_cache, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, ckpt_rows, stream);
+}
+
+int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream) {
+  if (!d_workspace) return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(d_workspace)) return LUMEN_ERR_MISALIGNED;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  WsHeader *hdr = static_cast<WsHeader *>(d_workspace);
+  int32_t code = 0;
+  static const int32_t zero = 0;
+  if (hipMemcpyAsync(&code, &hdr->err, sizeof(code), hipMemcpyDeviceToHost,
+                     s) != hipSuccess)
+    return LUMEN_ERR_HIP;
+  if (hipMemcpyAsync(&hdr->err, &zero, sizeof(zero), hipMemcpyHostToDevice,
+                     s) != hipSuccess)
+    return LUMEN_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return LUMEN_ERR_HIP;
+  return code;
+}
+
+const char *lumen_kv_ckpt_strerror(int code) {
+  switch (code) {
+    case LUMEN_OK: return "ok";
+    case LUMEN_ERR_INVALID_ARG: return "invalid argument";
+    case LUMEN_ERR_UNSUPPORTED: return "unsupported layout";
+    case LUMEN_ERR_MISALIGNED: return "buffer not 16-byte aligned";
+    case LUMEN_ERR_HIP: return "HIP runtime error";
+    case LUMEN_ERR_RANGE: return "token range outside the request or its block table";
+    case LUMEN_ERR_BLOCK_ID: return "block table entry outside the pool";
+    case LUMEN_ERR_CAPACITY: return "checkpoint row outside the checkpoint buffer";
+    default: return "unknown status";
+  }
+}
+
+int lumen_kv_ckpt_offload(const void *d_src, void *h_dst, size_t bytes,
+                          lumen_stream_t producer, lumen_stream_t side) {
+  if (bytes == 0) return LUMEN_OK;
+  if (!d_src || !h_dst) return LUMEN_ERR_INVALID_ARG;
+  DeviceInfo *dev = nullptr;
+  int st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  hipStream_t p = static_cast<hipStream_t>(producer);
+  hipStream_t q = static_cast<hipStream_t>(side);
+  {
+    // A wait captures the event's latest record at the time of the call, so
+    // one event per device serves every call.
+    std::lock_guard<std::mutex> lock(dev->event_mu);
+    if (hipEventRecord(dev->order_event, p) != hipSuccess ||
+        hipStreamWaitEvent(q, dev->order_event, 0) != hipSuccess)
+      return LUMEN_ERR_HIP;
+  }
+  if (hipMemcpyAsync(h_dst, d_src, bytes, hipMemcpyDeviceToHost, q) != hipSuccess)
+    return LUMEN_ERR_HIP;
+  return LUMEN_OK;
+}
+
+int lumen_kv_ckpt_stage_in(const void *h_src, void *d_dst, size_t bytes,
+                           lumen_stream_t side, lumen_stream_t consumer) {
+  if (bytes == 0) return LUMEN_OK;
+  if (!h_src || !d_dst) return LUMEN_ERR_INVALID_ARG;
+  DeviceInfo *dev = nullptr;
+  int st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  hipStream_t q = static_cast<hipStream_t>(side);
+  hipStream_t c = static_cast<hipStream_t>(consumer);
+  if (hipMemcpyAsync(d_dst, h_src, bytes, hipMemcpyHostToDevice, q) != hipSuccess)
+    return LUMEN_ERR_HIP;
+  std::lock_guard<std::mutex> lock(dev->event_mu);
+  if (hipEventRecord(dev->order_event, q) != hipSuccess ||
+      hipStreamWaitEvent(c, dev->order_event, 0) != hipSuccess)
+    return LUMEN_ERR_HIP;
+  return LUMEN_OK;
+}
+
+}  // extern "C"

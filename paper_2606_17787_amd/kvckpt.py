@@ -1,0 +1,265 @@
+"""Python binding of liblumen_kv_ckpt.so (ctypes; argument marshalling only).
+
+Each function has the name of the C entry point it calls and takes torch
+tensors for the device buffers; torch provides device memory, pinned host
+memory and streams, nothing else.  Every step of the path runs in the HIP
+library: if the library has not been built this module raises on first use
+rather than falling back to anything else.
+
+Before calling into the library, the binding checks that every tensor is on
+the right device, contiguous, of the right dtype and large enough for the
+sizes passed, because the C ABI sees only raw pointers.  Host-detected
+argument errors of the library raise LumenError; device-detected errors are
+returned by lumen_kv_ckpt_status.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Optional
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblumen_kv_ckpt.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "lumen_kv_ckpt.h")
+
+LUMEN_OK = 0
+LUMEN_ERR_INVALID_ARG = -1
+LUMEN_ERR_UNSUPPORTED = -2
+LUMEN_ERR_MISALIGNED = -3
+LUMEN_ERR_HIP = -4
+LUMEN_ERR_RANGE = -5
+LUMEN_ERR_BLOCK_ID = -6
+LUMEN_ERR_CAPACITY = -7
+LUMEN_CACHE_NHD = 0
+LUMEN_CACHE_HND = 1
+
+
+class LumenError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {lumen_kv_ckpt_strerror(code)} ({code})")
+
+
+class lumen_kv_layout(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32),
+                ("block_size", ctypes.c_int32),
+                ("num_blocks", ctypes.c_int64),
+                ("elem_bytes", ctypes.c_int32),
+                ("cache_order", ctypes.c_int32)]
+
+
+def exported_names():
+    """Entry points declared in include/lumen_kv_ckpt.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(lumen_kv_ckpt_\w+)\s*\(", text)))
+
+
+_LIB: Optional[ctypes.CDLL] = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    global _LIB
+    if _LIB is not None and path == LIB_PATH:
+        return _LIB
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build the HIP library first "
+            "(python -m paper_2606_17787_amd.build)")
+    lib = ctypes.CDLL(path)
+    p, i32, i64, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                       ctypes.c_size_t)
+    lay = ctypes.POINTER(lumen_kv_layout)
+    sigs = {
+        "lumen_kv_ckpt_plan_workspace_bytes": (sz, [i32]),
+        "lumen_kv_ckpt_plan": (ctypes.c_int, [p, p, i32, i64, p, p, p]),
+        "lumen_kv_ckpt_pack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
+        "lumen_kv_ckpt_unpack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
+        "lumen_kv_ckpt_status": (ctypes.c_int, [p, p]),
+        "lumen_kv_ckpt_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "lumen_kv_ckpt_offload": (ctypes.c_int, [p, p, sz, p, p]),
+        "lumen_kv_ckpt_stage_in": (ctypes.c_int, [p, p, sz, p, p]),
+    }
+    for name, (res, args) in sigs.items():
+        f = getattr(lib, name)
+        f.restype, f.argtypes = res, args
+    if path == LIB_PATH:
+        _LIB = lib
+    return lib
+
+
+# ------------------------------------------------------------ marshalling
+
+def layout(shape, num_blocks: int) -> lumen_kv_layout:
+    """lumen_kv_layout from a cache shape (num_layers, num_kv_heads,
+    head_dim, block_size, order 'NHD'/'HND', elem_bytes)."""
+    order = {"NHD": LUMEN_CACHE_NHD, "HND": LUMEN_CACHE_HND}[shape.order]
+    return lumen_kv_layout(shape.num_layers, shape.num_kv_heads,
+                           shape.head_dim, shape.block_size, int(num_blocks),
+                           getattr(shape, "elem_bytes", 2), order)
+
+
+def _stream_handle(stream: Optional[torch.cuda.Stream]):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: torch.Tensor, what: str, dtype=None) -> ctypes.c_void_p:
+    if not t.is_cuda:
+        raise ValueError(f"{what} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what} must be {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _check(code: int, where: str):
+    if code != LUMEN_OK:
+        raise LumenError(code, where)
+
+
+def _row_elems(shape) -> int:
+    return shape.num_layers * 2 * shape.num_kv_heads * shape.head_dim
+
+
+def _check_cache(shape, num_blocks: int, cache: torch.Tensor, what: str):
+    if cache.element_size() != 2:
+        raise ValueError(f"{what} must have 2-byte elements")
+    need = (shape.num_layers * 2 * int(num_blocks) * shape.block_size
+            * shape.num_kv_heads * shape.head_dim)
+    if cache.numel() != need:
+        raise ValueError(f"{what} has {cache.numel()} elements, the layout "
+                         f"needs {need}")
+
+
+def _check_tables(block_tables: torch.Tensor, num_reqs: int):
+    if block_tables.dim() != 2 or block_tables.shape[0] != num_reqs:
+        raise ValueError("block_tables must be [num_reqs, bt_cols]")
+
+
+# ------------------------------------------------------------- entry points
+
+def lumen_kv_ckpt_plan_workspace_bytes(num_reqs: int) -> int:
+    return int(load_library().lumen_kv_ckpt_plan_workspace_bytes(num_reqs))
+
+
+def lumen_kv_ckpt_strerror(code: int) -> str:
+    return load_library().lumen_kv_ckpt_strerror(code).decode()
+
+
+def new_workspace(num_reqs: int, device=None) -> torch.Tensor:
+    """Device workspace of the size a plan over num_reqs requests needs."""
+    n = lumen_kv_ckpt_plan_workspace_bytes(num_reqs)
+    return torch.zeros(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def lumen_kv_ckpt_plan(start: torch.Tensor, end: torch.Tensor,
+                       workspace: torch.Tensor, row_base: int = 0,
+                       req_row_base: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None) -> None:
+    R = start.numel()
+    if end.numel() != R:
+        raise ValueError("start and end differ in length")
+    ps = _dev(start, "start", torch.int32)
+    pe = _dev(end, "end", torch.int32)
+    pw = _dev(workspace, "workspace")
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    pb = None
+    if req_row_base is not None:
+        if req_row_base.numel() != R:
+            raise ValueError("req_row_base must have one entry per request")
+        pb = _dev(req_row_base, "req_row_base", torch.int64)
+    _check(load_library().lumen_kv_ckpt_plan(ps, pe, R, int(row_base), pb, pw,
+                                             _stream_handle(stream)),
+           "lumen_kv_ckpt_plan")
+
+
+def _copy(name: str, shape, num_blocks: int, cache: torch.Tensor,
+          block_tables: torch.Tensor, workspace: torch.Tensor,
+          ckpt: torch.Tensor, stream):
+    R = block_tables.shape[0] if block_tables.dim() == 2 else -1
+    _check_tables(block_tables, R)
+    _check_cache(shape, num_blocks, cache, "cache")
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    if ckpt.element_size() != 2 or ckpt.numel() % _row_elems(shape):
+        raise ValueError("checkpoint must hold whole rows of 2-byte elements")
+    rows = ckpt.numel() // _row_elems(shape)
+    lay = layout(shape, num_blocks)
+    f = getattr(load_library(), name)
+    _check(f(ctypes.byref(lay), _dev(cache, "cache"),
+             _dev(block_tables, "block_tables", torch.int32),
+             block_tables.shape[1], R, _dev(workspace, "workspace"),
+             _dev(ckpt, "ckpt"), rows, _stream_handle(stream)), name)
+
+
+def lumen_kv_ckpt_pack(shape, num_blocks: int, cache: torch.Tensor,
+                       block_tables: torch.Tensor, workspace: torch.Tensor,
+                       ckpt: torch.Tensor,
+                       stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Gather the planned token ranges of `cache` into `ckpt` rows
+    ([rows, L*2*H*D] 2-byte elements; rows = ckpt.numel() // row_elems)."""
+    _copy("lumen_kv_ckpt_pack", shape, num_blocks, cache, block_tables,
+          workspace, ckpt, stream)
+
+
+def lumen_kv_ckpt_unpack(shape, num_blocks: int, cache: torch.Tensor,
+                         block_tables: torch.Tensor, workspace: torch.Tensor,
+                         ckpt: torch.Tensor,
+                         stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Scatter the planned checkpoint rows of `ckpt` into `cache`."""
+    _copy("lumen_kv_ckpt_unpack", shape, num_blocks, cache, block_tables,
+          workspace, ckpt, stream)
+
+
+def lumen_kv_ckpt_status(workspace: torch.Tensor,
+                         stream: Optional[torch.cuda.Stream] = None) -> int:
+    return int(load_library().lumen_kv_ckpt_status(
+        _dev(workspace, "workspace"), _stream_handle(stream)))
+
+
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def lumen_kv_ckpt_offload(src: torch.Tensor, dst: torch.Tensor,
+                          nbytes: Optional[int] = None,
+                          producer: Optional[torch.cuda.Stream] = None,
+                          side: Optional[torch.cuda.Stream] = None) -> None:
+    """Copy the first `nbytes` of device tensor `src` into host tensor `dst`
+    (pinned for overlap) on stream `side`, after `producer`'s queued work."""
+    n = min(_nbytes(src), _nbytes(dst)) if nbytes is None else int(nbytes)
+    if n > _nbytes(src) or n > _nbytes(dst):
+        raise ValueError("nbytes exceeds a buffer")
+    if dst.is_cuda or not dst.is_contiguous():
+        raise ValueError("dst must be a contiguous host tensor")
+    _check(load_library().lumen_kv_ckpt_offload(
+        _dev(src, "src"), ctypes.c_void_p(dst.data_ptr()), n,
+        _stream_handle(producer), _stream_handle(side)),
+        "lumen_kv_ckpt_offload")
+
+
+def lumen_kv_ckpt_stage_in(src: torch.Tensor, dst: torch.Tensor,
+                           nbytes: Optional[int] = None,
+                           side: Optional[torch.cuda.Stream] = None,
+                           consumer: Optional[torch.cuda.Stream] = None) -> None:
+    """Copy the first `nbytes` of host tensor `src` into device tensor `dst`
+    on stream `side`; later work on `consumer` waits for it."""
+    n = min(_nbytes(src), _nbytes(dst)) if nbytes is None else int(nbytes)
+    if n > _nbytes(src) or n > _nbytes(dst):
+        raise ValueError("nbytes exceeds a buffer")
+    if src.is_cuda or not src.is_contiguous():
+        raise ValueError("src must be a contiguous host tensor")
+    _check(load_library().lumen_kv_ckpt_stage_in(
+        ctypes.c_void_p(src.data_ptr()), _dev(dst, "dst"), n,
+        _stream_handle(side), _stream_handle(consumer)),
+        "lumen_kv_ckpt_stage_in")

@@ -1,0 +1,89 @@
+"""Helpers shared by the GPU tests: run the HIP path and the CPU oracle on the
+same seeded inputs and hand back host copies for element-by-element
+comparison."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2606_17787_amd.kvckpt as kv
+
+SENTINEL = 0x5A5A
+
+
+def dev():
+    return torch.device("cuda:0")
+
+
+def h2d(a: np.ndarray) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev())
+
+
+def d2h16(t: torch.Tensor) -> np.ndarray:
+    return t.cpu().numpy().view(np.uint16)
+
+
+def gpu_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None, dst_pool=None,
+             bt_dst=None, row_base=0, req_row_base=None, ckpt_rows=None,
+             in_place=False):
+    """Plan + pack (+ unpack) on the GPU.  Returns (status, ckpt, dst_pool)
+    as host arrays (dst_pool None when no unpack was asked for).  in_place:
+    the unpack writes into the pool the pack read from."""
+    s = np.asarray(s, np.int32)
+    e = np.asarray(e, np.int32)
+    R = s.shape[0]
+    if ckpt_rows is None:
+        ckpt_rows = int(np.maximum(e.astype(np.int64) - s, 0).sum()) + row_base
+    row_elems = shape.token_row_elems
+    ck_h = np.full(max(ckpt_rows, 0) * row_elems, SENTINEL, np.uint16)
+    ck = h2d(ck_h)
+    ws = kv.new_workspace(R, dev())
+    rb = None if req_row_base is None else h2d(np.asarray(req_row_base, np.int64))
+    kv.lumen_kv_ckpt_plan(h2d(s), h2d(e), ws, row_base, rb)
+    src = h2d(src_pool)
+    kv.lumen_kv_ckpt_pack(shape, nb_src, src, h2d(np.asarray(bt, np.int32)),
+                          ws, ck)
+    dst = None
+    if dst_pool is not None:
+        dst = src if in_place else h2d(dst_pool)
+        kv.lumen_kv_ckpt_unpack(shape, nb_dst, dst,
+                                h2d(np.asarray(bt_dst, np.int32)), ws, ck)
+    st = kv.lumen_kv_ckpt_status(ws)
+    return (st, d2h16(ck).reshape(-1, row_elems),
+            None if dst is None else d2h16(dst))
+
+
+def oracle_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None,
+                dst_pool=None, bt_dst=None, row_base=0, req_row_base=None,
+                ckpt_rows=None):
+    s = np.asarray(s, np.int32)
+    e = np.asarray(e, np.int32)
+    if ckpt_rows is None:
+        ckpt_rows = int(np.maximum(e.astype(np.int64) - s, 0).sum()) + row_base
+    ck = np.full((ckpt_rows, shape.token_row_elems), SENTINEL, np.uint16)
+    st, ck = oracle.pack(shape, nb_src, src_pool, bt, s, e, row_base,
+                         req_row_base, ckpt=ck)
+    dst = None
+    if dst_pool is not None and st == oracle.OK:
+        dst = dst_pool.copy()
+        st = oracle.unpack(shape, nb_dst, dst, bt_dst, s, e, ck, row_base,
+                           req_row_base)
+    return st, ck, dst
+
+
+def assert_same(gpu, ref, what=""):
+    st_g, ck_g, dst_g = gpu
+    st_o, ck_o, dst_o = ref
+    assert st_g == st_o == 0, (what, st_g, st_o)
+    if not np.array_equal(ck_g, ck_o):
+        bad = np.argwhere(ck_g != ck_o)
+        raise AssertionError(f"{what}: checkpoint differs at {len(bad)} "
+                             f"elements, first (row, elem) {bad[:4].tolist()}")
+    if dst_o is not None:
+        if not np.array_equal(dst_g, dst_o):
+            bad = np.flatnonzero(dst_g != dst_o)
+            raise AssertionError(f"{what}: restored pool differs at "
+                                 f"{len(bad)} elements, first {bad[:4]}")

@@ -1,0 +1,125 @@
+"""The C ABI without a GPU: the library loads, exports every entry point its
+header declares, and rejects bad host-side arguments before any HIP call
+(the fake pointers below are never dereferenced)."""
+import ctypes
+
+import pytest
+
+import paper_2606_17787_amd.kvckpt as kv
+
+FAKE = ctypes.c_void_p(0x7F0000000000)       # 16-byte aligned, never touched
+FAKE_ODD = ctypes.c_void_p(0x7F0000000008)   # misaligned for 16 bytes
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return kv.load_library()
+
+
+def test_exports_every_declared_entry_point(lib):
+    names = kv.exported_names()
+    assert set(names) >= {"lumen_kv_ckpt_plan", "lumen_kv_ckpt_pack",
+                          "lumen_kv_ckpt_unpack", "lumen_kv_ckpt_status",
+                          "lumen_kv_ckpt_strerror",
+                          "lumen_kv_ckpt_plan_workspace_bytes",
+                          "lumen_kv_ckpt_offload", "lumen_kv_ckpt_stage_in"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    with pytest.raises(RuntimeError, match="build the HIP library"):
+        kv.load_library(str(tmp_path / "absent.so"))
+
+
+def test_strerror(lib):
+    for code in range(-7, 1):
+        assert kv.lumen_kv_ckpt_strerror(code) not in ("", "unknown status")
+    assert kv.lumen_kv_ckpt_strerror(-99) == "unknown status"
+
+
+def test_workspace_bytes():
+    assert kv.lumen_kv_ckpt_plan_workspace_bytes(-1) == 0
+    prev = 0
+    for R in (0, 1, 2, 7, 256, 1024, 100000):
+        n = kv.lumen_kv_ckpt_plan_workspace_bytes(R)
+        assert n % 16 == 0 and n > prev
+        assert n >= 64 + 8 * (R + 1) + 8 * R + 4 * R
+        prev = n
+
+
+def _layout(**kw):
+    d = dict(num_layers=2, num_kv_heads=2, head_dim=64, block_size=16,
+             num_blocks=8, elem_bytes=2, cache_order=kv.LUMEN_CACHE_NHD)
+    d.update(kw)
+    return kv.lumen_kv_layout(**d)
+
+
+@pytest.mark.parametrize("fn", ["lumen_kv_ckpt_pack", "lumen_kv_ckpt_unpack"])
+def test_copy_host_validation(lib, fn):
+    f = getattr(lib, fn)
+
+    def call(lay=None, cache=FAKE, bt=FAKE, cols=4, R=2, ws=FAKE, ck=FAKE,
+             rows=100):
+        lay = _layout() if lay is None else lay
+        return f(ctypes.byref(lay) if lay is not False else None, cache, bt,
+                 cols, R, ws, ck, rows, None)
+
+    assert call(lay=False) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(num_layers=0)) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(num_kv_heads=-1)) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(block_size=0)) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(num_blocks=-1)) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(elem_bytes=4)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(lay=_layout(cache_order=2)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(lay=_layout(head_dim=4)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(lay=_layout(head_dim=12)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(R=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(cols=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(rows=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ws=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ws=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+    assert call(R=0, cache=None, bt=None, ck=None) == kv.LUMEN_OK
+    assert call(cache=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(bt=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ck=None) == kv.LUMEN_ERR_INVALID_ARG
+    # null is an error only for a non-empty buffer; empty ones pass on to
+    # the device (checked here only up to the first HIP call, which fails
+    # without a GPU)
+    assert call(ck=None, rows=0) in (kv.LUMEN_OK, kv.LUMEN_ERR_HIP)
+    assert call(bt=None, cols=0) in (kv.LUMEN_OK, kv.LUMEN_ERR_HIP)
+    assert call(cache=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+    assert call(ck=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+
+
+def test_plan_host_validation(lib):
+    f = lib.lumen_kv_ckpt_plan
+    assert f(FAKE, FAKE, -1, 0, None, FAKE, None) == kv.LUMEN_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 2, 0, None, None, None) == kv.LUMEN_ERR_INVALID_ARG
+    assert f(None, FAKE, 2, 0, None, FAKE, None) == kv.LUMEN_ERR_INVALID_ARG
+    assert f(FAKE, None, 2, 0, None, FAKE, None) == kv.LUMEN_ERR_INVALID_ARG
+    assert f(FAKE, FAKE, 2, 0, None, FAKE_ODD, None) == kv.LUMEN_ERR_MISALIGNED
+
+
+def test_status_and_copies_host_validation(lib):
+    assert lib.lumen_kv_ckpt_status(None, None) == kv.LUMEN_ERR_INVALID_ARG
+    assert lib.lumen_kv_ckpt_status(FAKE_ODD, None) == kv.LUMEN_ERR_MISALIGNED
+    for f in (lib.lumen_kv_ckpt_offload, lib.lumen_kv_ckpt_stage_in):
+        assert f(FAKE, FAKE, 0, None, None) == kv.LUMEN_OK
+        assert f(None, FAKE, 16, None, None) == kv.LUMEN_ERR_INVALID_ARG
+        assert f(FAKE, None, 16, None, None) == kv.LUMEN_ERR_INVALID_ARG
+
+
+def test_binding_checks_shapes_before_calling():
+    """The binding rejects host tensors and mis-sized buffers itself."""
+    import torch
+    from paper_2606_17787_amd.workloads import CacheShape
+    sh = CacheShape(2, 2, 64, 16)
+    cpu = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        kv.lumen_kv_ckpt_plan(cpu, cpu, torch.zeros(256, dtype=torch.uint8))
+    with pytest.raises(ValueError):
+        kv.lumen_kv_ckpt_pack(sh, 8, torch.zeros(10, dtype=torch.int16),
+                              torch.zeros(2, 4, dtype=torch.int32),
+                              torch.zeros(256, dtype=torch.uint8),
+                              torch.zeros(512, dtype=torch.int16))

@@ -1,0 +1,230 @@
+"""GPU path vs the CPU oracle, element by element (bit-exact: the path is a
+pure copy).  Sizes here let the oracle finish in seconds while spanning many
+wavefront spans, partial blocks and ragged tails; full-size workloads are in
+test_gpu_fullsize.py."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_17787_amd.kvckpt as kv
+from paper_2606_17787_amd import workloads as W
+from paper_2606_17787_amd.workloads import CacheShape, HND, NHD
+
+from gpu_util import assert_same, gpu_path, oracle_path, h2d, d2h16, dev
+
+pytestmark = pytest.mark.gpu
+
+
+def test_smoke():
+    import __graft_entry__
+    __graft_entry__.smoke()
+
+
+def test_tiny_workload_full_pack_and_restore():
+    w = W.c1_tiny()
+    rng = np.random.default_rng(101)
+    src = W.random_bits(rng, w.shape.pool_elems(w.num_blocks))
+    dst = W.random_bits(rng, w.shape.pool_elems(w.dst_num_blocks))
+    args = (w.shape, w.num_blocks, src, w.block_tables, w.starts[0],
+            w.ends[0], w.dst_num_blocks, dst, w.dst_block_tables)
+    assert_same(gpu_path(*args), oracle_path(*args), "tiny")
+
+
+SHAPES = [
+    CacheShape(1, 1, 8, 1, NHD), CacheShape(1, 1, 8, 1, HND),
+    CacheShape(2, 2, 64, 2, NHD), CacheShape(2, 2, 64, 3, HND),
+    CacheShape(5, 3, 24, 3, NHD), CacheShape(5, 3, 24, 3, HND),
+    CacheShape(2, 1, 128, 16, NHD), CacheShape(3, 4, 128, 16, HND),
+    CacheShape(2, 4, 64, 32, NHD), CacheShape(3, 2, 128, 32, HND),
+    CacheShape(4, 8, 128, 16, NHD), CacheShape(1, 3, 40, 5, HND),
+]
+
+
+def _case(rng, shape, R, max_tok, incremental, nb_extra=7):
+    bs = shape.block_size
+    cols = -(-max_tok // bs) + 1
+    nb = R * cols + nb_extra
+    perm = rng.permutation(nb).astype(np.int32)
+    bt = perm[:R * cols].reshape(R, cols)
+    bt2 = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    if incremental:
+        s = rng.integers(0, max_tok + 1, R)
+        e = np.minimum(s + rng.integers(0, 3 * bs + 2, R), max_tok)
+    else:
+        s = np.zeros(R, np.int64)
+        e = rng.integers(0, max_tok + 1, R)
+    s, e = s.astype(np.int32), e.astype(np.int32)
+    empty = rng.random(R) < 0.15
+    e[empty] = s[empty]
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    return nb, bt, bt2, s, e, src, dst
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"L{s.num_layers}H{s.num_kv_heads}D{s.head_dim}bs{s.block_size}{s.order}")
+@pytest.mark.parametrize("incremental", [False, True])
+def test_random_shapes(shape, incremental):
+    rng = np.random.default_rng(zlib.crc32(f"{shape}{incremental}".encode()))
+    for R, max_tok in ((1, 5), (3, 40), (17, 100)):
+        nb, bt, bt2, s, e, src, dst = _case(rng, shape, R, max_tok,
+                                            incremental)
+        args = (shape, nb, src, bt, s, e, nb, dst, bt2)
+        assert_same(gpu_path(*args), oracle_path(*args),
+                    f"R={R} packed")
+        # rows placed after an offset, with spare rows that stay untouched
+        n = int((e - s).sum())
+        kw = dict(row_base=3, ckpt_rows=n + 6)
+        assert_same(gpu_path(*args, **kw), oracle_path(*args, **kw),
+                    f"R={R} row_base")
+        # per-request reserved regions: token t of r at row base[r] + t
+        base = np.arange(R, dtype=np.int64) * (max_tok + 2)
+        kw = dict(req_row_base=base, ckpt_rows=R * (max_tok + 2))
+        assert_same(gpu_path(*args, **kw), oracle_path(*args, **kw),
+                    f"R={R} per-request")
+
+
+def test_empty_plan_and_all_empty_ranges():
+    shape = CacheShape(2, 2, 64, 16, NHD)
+    rng = np.random.default_rng(5)
+    nb = 8
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    bt = np.arange(8, dtype=np.int32).reshape(4, 2)
+    s = np.array([3, 0, 31, 7], np.int32)
+    args = (shape, nb, src, bt, s, s, nb, dst, bt)
+    assert_same(gpu_path(*args, ckpt_rows=2), oracle_path(*args, ckpt_rows=2),
+                "all empty")
+
+
+ERROR_CASES = [
+    # (start, end, bt, ckpt_rows, row_base, req_row_base)
+    ([0, 0], [12, 8], None, 20, 0, None),
+    ([0, 0], [13, 8], None, 64, 0, None),
+    ([0, 0], [12, 9], None, 64, 0, None),
+    ([3, 0], [2, 8], None, 64, 0, None),
+    ([-1, 0], [2, 8], None, 64, 0, None),
+    ([0, 0], [8, 1], [[0, 8, 2], [3, 4, -1]], 64, 0, None),
+    ([0, 0], [4, 1], [[0, 8, 2], [3, 4, -1]], 64, 0, None),
+    ([0, 0], [12, 8], None, 19, 0, None),
+    ([0, 0], [12, 8], None, 25, 6, None),
+    ([2, 0], [4, 1], None, 100, 0, [-3, 0]),
+    ([0, 0], [13, 9], None, 1, 0, None),
+    ([5, 0], [4, 9], None, 64, 0, None),
+]
+
+
+@pytest.mark.parametrize("case", range(len(ERROR_CASES)))
+def test_device_error_codes_match_oracle(case):
+    s, e, bt, rows, base, rb = ERROR_CASES[case]
+    shape = CacheShape(2, 2, 8, 4, NHD)
+    nb = 8
+    bt = np.array(bt if bt is not None else [[0, 1, 2], [3, 4, -1]], np.int32)
+    rng = np.random.default_rng(case)
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    ck = np.zeros(((rows + 8), shape.token_row_elems), np.uint16)
+    st_o, _ = oracle.pack(shape, nb, src, bt, s, e, base, rb, ckpt=ck,
+                          ckpt_rows=rows)
+    st_g, _, _ = gpu_path(shape, nb, src, bt, s, e, row_base=base,
+                          req_row_base=rb, ckpt_rows=rows)
+    assert st_g == st_o, (st_g, st_o)
+    # a fresh plan starts a new error epoch and a clean run reports OK
+    st_g, _, _ = gpu_path(shape, nb, src, np.array([[0, 1, 2], [3, 4, 5]],
+                                                   np.int32), [0, 0], [1, 1])
+    assert st_g == kv.LUMEN_OK
+
+
+def test_status_clears_the_error_word():
+    shape = CacheShape(1, 1, 8, 4, NHD)
+    nb = 2
+    src = h2d(np.zeros(shape.pool_elems(nb), np.uint16))
+    ws = kv.new_workspace(1, dev())
+    kv.lumen_kv_ckpt_plan(h2d(np.array([0], np.int32)),
+                          h2d(np.array([4], np.int32)), ws)
+    ck = torch.zeros(4 * shape.token_row_elems, dtype=torch.int16,
+                     device=dev())
+    kv.lumen_kv_ckpt_pack(shape, nb, src, h2d(np.array([[5]], np.int32)),
+                          ws, ck)
+    assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_ERR_BLOCK_ID
+    assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK
+
+
+@pytest.mark.parametrize("make", [
+    lambda: W.c2_llama8b(num_reqs=9, steps=3, median=150, clip_hi=300),
+    lambda: W.c5_qwen_hnd(num_reqs=13, steps=3, median=100, clip_hi=200),
+], ids=["llama3-8b-decode-small", "qwen-gqa-hnd-small"])
+def test_reduced_incremental_workloads(make):
+    w = make()
+    rng = np.random.default_rng(202)
+    src = W.random_bits(rng, w.shape.pool_elems(w.num_blocks))
+    dst = W.random_bits(rng, w.shape.pool_elems(w.dst_num_blocks))
+    g_dst, o_dst = dst, dst
+    for k in range(w.num_steps):
+        gpu = gpu_path(w.shape, w.num_blocks, src, w.block_tables, w.starts[k],
+                       w.ends[k], w.dst_num_blocks, g_dst, w.dst_block_tables)
+        ref = oracle_path(w.shape, w.num_blocks, src, w.block_tables,
+                          w.starts[k], w.ends[k], w.dst_num_blocks, o_dst,
+                          w.dst_block_tables)
+        assert_same(gpu, ref, f"step {k}")
+        g_dst, o_dst = gpu[2], ref[2]
+
+
+def test_reduced_tp8_shard_in_place():
+    w = W.c4_llama70b_tp8(num_reqs=11, median=120, clip_hi=400)
+    rng = np.random.default_rng(303)
+    pool = W.random_bits(rng, w.shape.pool_elems(w.num_blocks))
+    # pack, then unpack into the same pool under a fresh permutation
+    args = (w.shape, w.num_blocks, pool, w.block_tables, w.starts[0],
+            w.ends[0], w.num_blocks, pool, w.dst_block_tables)
+    assert_same(gpu_path(*args, in_place=True), oracle_path(*args),
+                "in place")
+
+
+def test_reduced_restore_burst():
+    w = W.c3_restore(num_reqs=5, ctx_lo=40, ctx_hi=300, pool_blocks=200)
+    rng = np.random.default_rng(404)
+    n = w.step_tokens(0)
+    ck = W.random_bits(rng, n * w.shape.token_row_elems)
+    pool = W.random_bits(rng, w.shape.pool_elems(w.dst_num_blocks))
+    for wave in W.restore_waves(w):
+        s, e = w.starts[0][wave], w.ends[0][wave]
+        bt = w.dst_block_tables[wave]
+        rows = int((e - s).sum())
+        off = int(w.ends[0][:wave[0]].sum())
+        ck_w = ck[off * w.shape.token_row_elems:(off + rows) * w.shape.token_row_elems]
+        # GPU: unpack only
+        ws = kv.new_workspace(len(wave), dev())
+        kv.lumen_kv_ckpt_plan(h2d(s), h2d(e), ws)
+        d = h2d(pool)
+        kv.lumen_kv_ckpt_unpack(w.shape, w.dst_num_blocks, d, h2d(bt), ws,
+                                h2d(ck_w))
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+        ref = pool.copy()
+        assert oracle.unpack(w.shape, w.dst_num_blocks, ref, bt, s, e,
+                             ck_w.reshape(rows, -1)) == 0
+        assert np.array_equal(d2h16(d), ref)
+
+
+def test_offload_and_stage_in_bytes():
+    rng = np.random.default_rng(9)
+    a = W.random_bits(rng, 3 << 20)
+    d = h2d(a)
+    host = torch.empty(a.size, dtype=torch.int16, pin_memory=True)
+    side = torch.cuda.Stream()
+    kv.lumen_kv_ckpt_offload(d, host, producer=torch.cuda.current_stream(),
+                             side=side)
+    side.synchronize()
+    assert np.array_equal(host.numpy().view(np.uint16), a)
+    back = torch.zeros_like(d)
+    kv.lumen_kv_ckpt_stage_in(host, back, side=side,
+                              consumer=torch.cuda.current_stream())
+    torch.cuda.current_stream().synchronize()
+    assert np.array_equal(d2h16(back), a)
+    # partial copy of the first bytes only
+    host.zero_()
+    kv.lumen_kv_ckpt_offload(d, host, nbytes=1000, side=side)
+    side.synchronize()
+    got = host.numpy().view(np.uint16)
+    assert np.array_equal(got[:500], a[:500]) and not got[500:].any()

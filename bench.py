@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU oracle sample")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB "
+                    "(5 times), the reference for HBM byte counters")
     return ap.parse_args()
 
 
@@ -232,6 +235,24 @@ def offload_leg(torch, kv):
     return dict(d2h_GBps=gb(n) / dt, bytes=n, ok=ok)
 
 
+def calibrate_copy(torch, mib):
+    """A plain device-to-device copy of known size: read + write bytes are
+    exactly 2 * mib MiB per launch, the scale for the FETCH_SIZE/WRITE_SIZE
+    counters of the checkpoint kernels."""
+    n = mib << 20
+    a = torch.empty(n // 2, dtype=torch.int16, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / 5
+    print(json.dumps({"calibration_copy_bytes": n,
+                      "copy_GBps": round(2 * n / dt / 1e9, 1)}), flush=True)
+
+
 # ------------------------------------------------------------ CPU baseline
 
 def cpu_baseline(W, seconds):
@@ -287,8 +308,11 @@ def main():
     import torch
     import paper_2606_17787_amd.kvckpt as kv
     from paper_2606_17787_amd import workloads as W
-    kv.load_library()
     torch.cuda.set_device(0)
+    if args.calibrate_copy_mib:
+        calibrate_copy(torch, args.calibrate_copy_mib)
+        return
+    kv.load_library()
 
     dec = decode_leg(torch, kv, W, args.steps, args.warmup)
     w = dec.pop("workload")

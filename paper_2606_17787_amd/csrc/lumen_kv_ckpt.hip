@@ -30,12 +30,46 @@
 
 namespace {
 
+// Tuning knobs (compile-time): threads per workgroup of the copy kernels,
+// 16-byte vectors each lane keeps in flight, and non-temporal hints on the
+// loads (bit 0) and stores (bit 1) of the gather and of the scatter.
+#ifndef LUMEN_KV_CKPT_BLOCK_THREADS
+#define LUMEN_KV_CKPT_BLOCK_THREADS 256
+#endif
+#ifndef LUMEN_KV_CKPT_UNROLL
+#define LUMEN_KV_CKPT_UNROLL 4
+#endif
+#ifndef LUMEN_KV_CKPT_PACK_NT
+#define LUMEN_KV_CKPT_PACK_NT 3
+#endif
+#ifndef LUMEN_KV_CKPT_UNPACK_NT
+#define LUMEN_KV_CKPT_UNPACK_NT 3
+#endif
+#ifndef LUMEN_KV_CKPT_WAVES_PER_CU
+#define LUMEN_KV_CKPT_WAVES_PER_CU 32
+#endif
+// Waves per SIMD the register allocation of the copy kernels must allow
+// (0: compiler's choice).
+// Double-buffer the batches of a row segment (1) or not (0).
+#ifndef LUMEN_KV_CKPT_PIPELINE
+#define LUMEN_KV_CKPT_PIPELINE 1
+#endif
+#ifndef LUMEN_KV_CKPT_WAVES_PER_EU
+#define LUMEN_KV_CKPT_WAVES_PER_EU 0
+#endif
+#if LUMEN_KV_CKPT_WAVES_PER_EU > 0
+#define LUMEN_COPY_OCCUPANCY \
+  __attribute__((amdgpu_waves_per_eu(LUMEN_KV_CKPT_WAVES_PER_EU)))
+#else
+#define LUMEN_COPY_OCCUPANCY
+#endif
+
 constexpr int kWave = 64;
-constexpr int kBlockThreads = 256;
+constexpr int kBlockThreads = LUMEN_KV_CKPT_BLOCK_THREADS;
 constexpr int kWavesPerBlock = kBlockThreads / kWave;
 constexpr int kPlanThreads = 1024;
-constexpr int kUnroll = 8;  // 16-byte vectors in flight per lane
-constexpr int kDefaultWavesPerCU = 16;
+constexpr int kUnroll = LUMEN_KV_CKPT_UNROLL;
+constexpr int kDefaultWavesPerCU = LUMEN_KV_CKPT_WAVES_PER_CU;
 
 // Workspace layout (device memory, caller-owned):
 //   WsHeader, then int64 prefix[R+1], int64 first_row[R], int32 start[R].
@@ -143,17 +177,47 @@ __device__ __forceinline__ int64_t cache_vec_offset(uint32_t vv,
   return off;
 }
 
-// One batch of kUnroll vectors per lane: all loads first, then all stores,
-// so each lane keeps kUnroll 16-byte requests in flight.  kPred guards the
-// last, partial batch of a row segment.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load / store.  The buffer between them is a uint4 struct: an
+// array of clang vector types in copy_batch makes the register allocator
+// keep far more live values (256 VGPRs instead of about 70).
+template <bool kNt>
+__device__ __forceinline__ uint4 load16(const uint8_t *p) {
+  if (kNt) {
+    const u32x4 v =
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
+  return *reinterpret_cast<const uint4 *>(p);
+}
+
+template <bool kNt>
+__device__ __forceinline__ void store16(uint8_t *p, const uint4 &v) {
+  if (kNt)
+    __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w},
+                                reinterpret_cast<u32x4 *>(p));
+  else
+    *reinterpret_cast<uint4 *>(p) = v;
+}
+
+// Loads and stores of one batch: kUnroll 16-byte vectors per lane, the
+// lanes of a wavefront covering kWave consecutive vectors per step.  kPred
+// guards the last, partial batch of a row segment.
+template <bool kPack>
+constexpr int nt_policy() {
+  // Measured on the decode workload, each kernel in a loop of its own:
+  // non-temporal loads and stores are fastest for both directions.
+  return kPack ? LUMEN_KV_CKPT_PACK_NT : LUMEN_KV_CKPT_UNPACK_NT;
+}
+
 template <bool kPack, bool kHeadMajor, bool kPred>
-__device__ __forceinline__ void copy_batch(const uint8_t *__restrict__ src,
-                                           uint8_t *__restrict__ dst,
+__device__ __forceinline__ void load_batch(uint4 (&buf)[kUnroll],
+                                           const uint8_t *__restrict__ src,
                                            int64_t cache_tok, int64_t ckpt_off,
                                            uint32_t vbase, int32_t v0,
                                            int32_t nvec, int lane,
                                            const Geom &g) {
-  uint4 buf[kUnroll];
 #pragma unroll
   for (int k = 0; k < kUnroll; ++k) {
     const int32_t v = v0 + k * kWave + lane;
@@ -162,9 +226,18 @@ __device__ __forceinline__ void copy_batch(const uint8_t *__restrict__ src,
       const int64_t off =
           kPack ? cache_tok + cache_vec_offset<kHeadMajor>(vbase + v, g)
                 : ckpt_off + int64_t(v) * 16;
-      buf[k] = *reinterpret_cast<const uint4 *>(src + off);
+      buf[k] = load16<(nt_policy<kPack>() & 1) != 0>(src + off);
     }
   }
+}
+
+template <bool kPack, bool kHeadMajor, bool kPred>
+__device__ __forceinline__ void store_batch(const uint4 (&buf)[kUnroll],
+                                            uint8_t *__restrict__ dst,
+                                            int64_t cache_tok, int64_t ckpt_off,
+                                            uint32_t vbase, int32_t v0,
+                                            int32_t nvec, int lane,
+                                            const Geom &g) {
 #pragma unroll
   for (int k = 0; k < kUnroll; ++k) {
     const int32_t v = v0 + k * kWave + lane;
@@ -172,15 +245,89 @@ __device__ __forceinline__ void copy_batch(const uint8_t *__restrict__ src,
       const int64_t off =
           kPack ? ckpt_off + int64_t(v) * 16
                 : cache_tok + cache_vec_offset<kHeadMajor>(vbase + v, g);
-      *reinterpret_cast<uint4 *>(dst + off) = buf[k];
+      store16<(nt_policy<kPack>() & 2) != 0>(dst + off, buf[k]);
     }
   }
+}
+
+// Copies vectors [0, nvec) of a row segment.  With LUMEN_KV_CKPT_PIPELINE the
+// full batches are double-buffered: the loads of batch i+1 are issued before
+// the stores of batch i, so a wavefront never waits for its own stores
+// before loading again and keeps two batches of loads in flight.
+template <bool kPack, bool kHeadMajor>
+__device__ __forceinline__ void copy_segment(const uint8_t *__restrict__ src,
+                                             uint8_t *__restrict__ dst,
+                                             int64_t cache_tok,
+                                             int64_t ckpt_off, uint32_t vbase,
+                                             int32_t nvec, int lane,
+                                             const Geom &g) {
+  constexpr int32_t kBatch = kWave * kUnroll;
+  const int32_t nfull = nvec / kBatch;
+  uint4 a[kUnroll];
+#if LUMEN_KV_CKPT_PIPELINE
+  if (nfull > 0) {
+    uint4 b[kUnroll];
+    load_batch<kPack, kHeadMajor, false>(a, src, cache_tok, ckpt_off, vbase,
+                                         0, nvec, lane, g);
+    int32_t i = 0;
+    while (true) {
+      if (i + 1 < nfull)
+        load_batch<kPack, kHeadMajor, false>(b, src, cache_tok, ckpt_off,
+                                             vbase, (i + 1) * kBatch, nvec,
+                                             lane, g);
+      store_batch<kPack, kHeadMajor, false>(a, dst, cache_tok, ckpt_off,
+                                            vbase, i * kBatch, nvec, lane, g);
+      if (++i >= nfull) break;
+      if (i + 1 < nfull)
+        load_batch<kPack, kHeadMajor, false>(a, src, cache_tok, ckpt_off,
+                                             vbase, (i + 1) * kBatch, nvec,
+                                             lane, g);
+      store_batch<kPack, kHeadMajor, false>(b, dst, cache_tok, ckpt_off,
+                                            vbase, i * kBatch, nvec, lane, g);
+      if (++i >= nfull) break;
+    }
+  }
+#else
+  for (int32_t i = 0; i < nfull; ++i) {
+    load_batch<kPack, kHeadMajor, false>(a, src, cache_tok, ckpt_off, vbase,
+                                         i * kBatch, nvec, lane, g);
+    store_batch<kPack, kHeadMajor, false>(a, dst, cache_tok, ckpt_off, vbase,
+                                          i * kBatch, nvec, lane, g);
+  }
+#endif
+  if (nfull * kBatch < nvec) {
+    load_batch<kPack, kHeadMajor, true>(a, src, cache_tok, ckpt_off, vbase,
+                                        nfull * kBatch, nvec, lane, g);
+    store_batch<kPack, kHeadMajor, true>(a, dst, cache_tok, ckpt_off, vbase,
+                                         nfull * kBatch, nvec, lane, g);
+  }
+}
+
+// Index of the block-table entry holding token t of request r.  A page past
+// the table is clamped to the table's last column (so the load stays in
+// bounds and can be issued unconditionally) and reported through `past`.
+__device__ __forceinline__ int64_t entry_index(int32_t r, int64_t t,
+                                               const Geom &g, bool &past) {
+  const uint32_t page = fdiv(uint32_t(t), g.div_bs);
+  past = page >= uint32_t(g.bt_cols);
+  return int64_t(r) * g.bt_cols + min(page, uint32_t(g.bt_cols - 1));
+}
+
+// Status of a token row, checked in the documented order: page inside the
+// block table (RANGE), entry a block of the pool (BLOCK_ID), checkpoint row
+// inside the buffer (CAPACITY).
+__device__ __forceinline__ int row_status(bool past, int32_t entry,
+                                          int64_t crow, const Geom &g) {
+  if (past) return LUMEN_ERR_RANGE;
+  if (entry < 0 || entry >= g.num_blocks) return LUMEN_ERR_BLOCK_ID;
+  if (crow < 0 || crow >= g.ckpt_rows) return LUMEN_ERR_CAPACITY;
+  return LUMEN_OK;
 }
 
 // One persistent kernel for both directions.  kPack: cache -> checkpoint;
 // otherwise checkpoint -> cache.
 template <bool kPack, bool kHeadMajor>
-__global__ __launch_bounds__(kBlockThreads) void copy_rows_kernel(
+__global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_kernel(
     const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
     const int32_t *__restrict__ block_tables,
     const WsHeader *__restrict__ hdr, const int64_t *__restrict__ prefix,
@@ -203,68 +350,84 @@ __global__ __launch_bounds__(kBlockThreads) void copy_rows_kernel(
 
   // First token row of the span and the request that owns it: the last
   // request whose prefix does not exceed the row (empty requests share
-  // their successor's prefix and are skipped by taking the last).
+  // their successor's prefix and are skipped by taking the last).  A 64-way
+  // search, one vector load per level, keeps the chain of dependent loads
+  // before the first copy short (two levels up to 4096 requests).
   int64_t row = u / L;
   int32_t l0 = int32_t(u - row * L);
-  int32_t lo = 0, hi = g.num_reqs - 1;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi + 1) >> 1;
-    if (prefix[mid] <= row) lo = mid; else hi = mid - 1;
+  int32_t lo = 0, n = g.num_reqs;
+  while (n > 1) {
+    const int32_t step = (n + kWave - 1) / kWave;
+    const int32_t off = lane * step;
+    const int64_t p = off < n ? prefix[lo + off] : INT64_MAX;
+    const int32_t c = __popcll(__ballot(p <= row));  // >= 1: prefix[lo] <= row
+    lo += (c - 1) * step;
+    n = min(step, n - (c - 1) * step);
   }
   int32_t r = lo;
+  const int64_t p0 = prefix[r];
   int64_t row_end = prefix[r + 1];
-  int64_t t = start[r] + (row - prefix[r]);
-  int64_t crow = first_row[r] + (row - prefix[r]);
+  int64_t t = start[r] + (row - p0);
+  int64_t crow = first_row[r] + (row - p0);
+  if (g.bt_cols == 0) {  // every page lies past an empty table
+    record_error(err, LUMEN_ERR_RANGE);
+    return;
+  }
+  bool past;
+  int32_t b = block_tables[entry_index(r, t, g, past)];
 
   while (true) {
     const int32_t nl = int32_t(min(int64_t(g.num_layers - l0), u_end - u));
-    const uint32_t page = fdiv(uint32_t(t), g.div_bs);
-    const uint32_t slot = uint32_t(t) - page * uint32_t(g.block_size);
-    int code = LUMEN_OK;
-    int64_t b = -1;
-    if (page >= uint32_t(g.bt_cols)) {
-      code = LUMEN_ERR_RANGE;
-    } else {
-      b = block_tables[int64_t(r) * g.bt_cols + page];
-      if (b < 0 || b >= g.num_blocks)
-        code = LUMEN_ERR_BLOCK_ID;
-      else if (crow < 0 || crow >= g.ckpt_rows)
-        code = LUMEN_ERR_CAPACITY;
+    const bool more = u + nl < u_end;
+    const int code = row_status(past, b, crow, g);
+    // Cache side: (block, slot) of layer 0 / K; checkpoint side: the span's
+    // first unit in this row.
+    const uint32_t slot = uint32_t(t) - fdiv(uint32_t(t), g.div_bs) *
+                                            uint32_t(g.block_size);
+    const int64_t cache_tok =
+        int64_t(b) * g.block_bytes + int64_t(slot) * g.slot_bytes;
+    const int64_t ckpt_off =
+        crow * g.row_bytes + int64_t(l0) * g.unit_vecs * 16;
+    // Materialise this row's addresses here: otherwise the compiler sinks
+    // their arithmetic below the next row's block-table load, and the wait
+    // for this row's entry then also waits for that load.
+    asm volatile("" ::"s"(cache_tok), "s"(ckpt_off) : "memory");
+
+    // Position and block-table entry of the next row.  The entry is loaded
+    // unconditionally (clamped index), after every use of this row's entry
+    // and before this row's copy, and first used after that copy: the scalar
+    // load overlaps with the copy instead of stalling the next row.
+    int32_t r2 = r;
+    int64_t row_end2 = row_end, t2 = t + 1, crow2 = crow + 1;
+    if (more && row + 1 == row_end) {
+      // Next request with rows; one exists because row + 1 < total_rows.
+      do {
+        ++r2;
+      } while (prefix[r2 + 1] == row + 1);
+      row_end2 = prefix[r2 + 1];
+      t2 = start[r2];
+      crow2 = first_row[r2];
     }
+    bool past2;
+    const int32_t b2 = block_tables[entry_index(r2, t2, g, past2)];
+
     if (code != LUMEN_OK) {
       record_error(err, code);
     } else {
-      // Cache side: (block, slot) of layer 0 / K; checkpoint side: the
-      // span's first unit in this row.
-      const int64_t cache_tok = b * g.block_bytes + int64_t(slot) * g.slot_bytes;
-      const int64_t ckpt_off =
-          crow * g.row_bytes + int64_t(l0) * g.unit_vecs * 16;
-      const uint32_t vbase = uint32_t(l0) * uint32_t(g.unit_vecs);
-      const int32_t nvec = nl * g.unit_vecs;
-      constexpr int32_t kBatch = kWave * kUnroll;
-      int32_t v0 = 0;
-      for (; v0 + kBatch <= nvec; v0 += kBatch)
-        copy_batch<kPack, kHeadMajor, false>(src, dst, cache_tok, ckpt_off,
-                                             vbase, v0, nvec, lane, g);
-      if (v0 < nvec)
-        copy_batch<kPack, kHeadMajor, true>(src, dst, cache_tok, ckpt_off,
-                                            vbase, v0, nvec, lane, g);
+      copy_segment<kPack, kHeadMajor>(src, dst, cache_tok, ckpt_off,
+                                      uint32_t(l0) * uint32_t(g.unit_vecs),
+                                      nl * g.unit_vecs, lane, g);
     }
+    if (!more) break;
     u += nl;
-    if (u >= u_end) break;
     l0 = 0;
     ++row;
-    ++t;
-    ++crow;
-    if (row == row_end) {
-      // Next request with rows; one exists because row < total_rows.
-      do {
-        ++r;
-      } while (prefix[r + 1] == row);
-      row_end = prefix[r + 1];
-      t = start[r];
-      crow = first_row[r];
-    }
+    r = r2;
+    row_end = row_end2;
+    t = t2;
+    crow = crow2;
+    b = b2;
+    past = past2;
   }
 }
 

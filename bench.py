@@ -1,24 +1,30 @@
 #!/usr/bin/env python3
 """Benchmark of the paged-KV checkpoint path on one MI355X.
 
-One step = the hot path over one decode step of the Llama-3-8B-shaped
-workload (32 layers, 8 KV heads, head_dim 128, block 16, bf16; 256 requests
-with lognormal contexts; each step checkpoints every request's newest 1-16
-tokens):
+Headline step (the value and the roofline): one decode step of the
+Llama-3-8B-shaped workload (32 layers, 8 KV heads, head_dim 128, block 16,
+bf16; 256 requests with lognormal contexts; every step checkpoints each
+request's newest 1-16 tokens):
 
-    plan(step k)   -> pack(step k)   source pool -> checkpoint region k
-    plan(step k')  -> unpack(step k') checkpoint region k' -> restore pool
+    plan(step k)  -> pack(step k)    source pool -> checkpoint region k
+    plan(step k') -> unpack(step k') checkpoint region k' -> restore pool
 
 with k' = k + 50 (mod 100), so the restore reads a region written 50 steps
-(about 28 GB of traffic) earlier and cannot be served from the 256 MB
+(about 28 GB of traffic) earlier, never a copy still held in the 256 MB
 Infinity Cache.  Inputs (pools, block tables, ranges) are resident in HBM
 before timing; the device error word is checked after the timed loop.
 
-Printed: one JSON line with the whole-step throughput (pack + unpack bytes
-read + written / wall time), per-kernel GB/s from HIP events on the launch
-stream, the roofline fraction of the dominant kernel, the restore-burst leg
-(ms per restored request), a device->pinned-host leg, and the CPU oracle
-timed on a bounded sample of the same workload.
+Further legs (reported beside the headline, not part of its value):
+  * qwen-gqa-hnd    the same decode loop on the head-major Qwen-style cache
+  * restore-burst   64 interrupted requests restored into a 60%-occupied
+                    pool; ms per restored request
+  * tp8-shard       full pack and in-place unpack of one TP=8 rank of a
+                    Llama-3-70B-shaped cache, the packed rows streamed to a
+                    pinned host ring on a side stream during the pack
+  * cpu_baseline    the CPU oracle on a bounded sample of the decode workload
+
+Bytes are algorithmic: 2 x tokens x token_row_bytes (read + write),
+decimal GB; peak is MI355X's 8 TB/s.
 """
 from __future__ import annotations
 
@@ -36,6 +42,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
+ALL_LEGS = ("decode", "qwen", "restore", "tp8", "cpu")
 
 
 def parse():
@@ -43,11 +50,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--no-restore", action="store_true",
-                    help="skip the restore-burst leg")
-    ap.add_argument("--no-offload", action="store_true",
-                    help="skip the device->pinned-host leg")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--legs", default=",".join(ALL_LEGS),
+                    help="comma list of " + ",".join(ALL_LEGS))
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU oracle sample")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -60,11 +64,16 @@ def gb(x):
     return x / 1e9
 
 
+def say(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
 # --------------------------------------------------------------- GPU legs
 
-def decode_leg(torch, kv, W, steps, warmup):
+def incremental_leg(torch, kv, w, steps, warmup, seed):
+    """Decode loop: step i packs step k = i mod S and restores step
+    k + S/2; per-kernel times from HIP events on the launch stream."""
     dev = torch.device("cuda:0")
-    w = W.c2_llama8b()
     sh = w.shape
     S = w.num_steps
     rows = np.array([w.step_tokens(k) for k in range(S)], np.int64)
@@ -72,7 +81,7 @@ def decode_leg(torch, kv, W, steps, warmup):
     row_elems = sh.token_row_elems
 
     g = torch.Generator(device=dev)
-    g.manual_seed(2)
+    g.manual_seed(seed)
     src = torch.empty(sh.pool_elems(w.num_blocks), dtype=torch.bfloat16,
                       device=dev)
     src.normal_(generator=g)
@@ -107,7 +116,8 @@ def decode_leg(torch, kv, W, steps, warmup):
         if events: events[1].record()
         kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, int(row_off[k2]))
         if events: events[2].record()
-        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt_dst, ws_b, arena)
+        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt_dst, ws_b,
+                                arena)
         if events: events[3].record()
         return k, k2
 
@@ -140,24 +150,27 @@ def decode_leg(torch, kv, W, steps, warmup):
     roundtrip = bool(torch.equal(back.view(torch.int16),
                                  region.view(torch.int16)))
     assert kv.lumen_kv_ckpt_status(ws_b) == 0
+    del src, dst, arena, back
+    torch.cuda.empty_cache()
 
-    res = dict(
-        workload=w, wall_ms=wall_ms, steps=steps,
-        bytes_total=float(pack_b.sum() + unpack_b.sum()),
-        pack_GBps=gb(pack_b.sum()) / (pack_ms.sum() / 1e3),
-        unpack_GBps=gb(unpack_b.sum()) / (unpack_ms.sum() / 1e3),
-        pack_us_median=float(np.median(pack_ms) * 1e3),
-        unpack_us_median=float(np.median(unpack_ms) * 1e3),
+    pack_GBps = gb(pack_b.sum()) / (pack_ms.sum() / 1e3)
+    unpack_GBps = gb(unpack_b.sum()) / (unpack_ms.sum() / 1e3)
+    return dict(
+        workload=w.name, steps=steps, warmup=warmup,
+        wall_ms=wall_ms, ms_per_step=wall_ms / steps,
+        step_GBps=gb(pack_b.sum() + unpack_b.sum()) / (wall_ms / 1e3),
+        pack_GBps=pack_GBps, unpack_GBps=unpack_GBps,
+        pack_pct_peak=100 * pack_GBps / HBM_PEAK_GBPS,
+        unpack_pct_peak=100 * unpack_GBps / HBM_PEAK_GBPS,
         pack_us_mean=float(pack_ms.mean() * 1e3),
         unpack_us_mean=float(unpack_ms.mean() * 1e3),
+        pack_us_median=float(np.median(pack_ms) * 1e3),
+        unpack_us_median=float(np.median(unpack_ms) * 1e3),
         pack_bytes_mean=float(pack_b.mean()),
         unpack_bytes_mean=float(unpack_b.mean()),
         tokens_per_step_mean=float(rows.mean()),
         roundtrip_ok=roundtrip,
     )
-    del src, dst, arena
-    torch.cuda.empty_cache()
-    return res
 
 
 def restore_leg(torch, kv, W):
@@ -201,38 +214,134 @@ def restore_leg(torch, kv, W):
         assert kv.lumen_kv_ckpt_status(ws) == 0
         t = float(np.median(reps))
         byts = 2.0 * nrows * sh.token_row_bytes
-        wave_stats.append(dict(requests=len(wv), tokens=nrows, ms=t,
-                               GBps=gb(byts) / (t / 1e3)))
+        wave_stats.append(dict(requests=len(wv), tokens=nrows, ms=round(t, 3),
+                               GBps=round(gb(byts) / (t / 1e3), 1)))
         per_req_ms += [t * float(ctx[r]) / nrows for r in wv]
     del pool, ck
     torch.cuda.empty_cache()
     tot_ms = sum(x["ms"] for x in wave_stats)
     tot_b = sum(2.0 * x["tokens"] * sh.token_row_bytes for x in wave_stats)
-    return dict(restore_ms_per_request=tot_ms / w.num_reqs,
+    return dict(workload=w.name, requests=w.num_reqs,
+                restore_ms_per_request=tot_ms / w.num_reqs,
                 restore_ms_per_request_median=float(np.median(per_req_ms)),
-                restore_GBps=gb(tot_b) / (tot_ms / 1e3),
-                waves=wave_stats, requests=w.num_reqs,
-                mean_request_GB=gb(float(ctx.mean()) * sh.token_row_bytes))
+                unpack_GBps=gb(tot_b) / (tot_ms / 1e3),
+                mean_request_GB=gb(float(ctx.mean()) * sh.token_row_bytes),
+                waves=wave_stats)
 
 
-def offload_leg(torch, kv):
-    """Device -> pinned host over the side stream (2 GiB), the first stage of
-    shipping a checkpoint off the GPU."""
+def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
+    """One TP=8 rank's shard of a Llama-3-70B-shaped cache: full pack in
+    request chunks, each chunk's rows streamed to a ring of pinned host
+    buffers on a side stream as soon as the chunk is packed; the pack alone
+    first (its slowdown under the concurrent D2H), then an in-place unpack
+    under a fresh permutation."""
     dev = torch.device("cuda:0")
-    n = 2 << 30
-    d = torch.empty(n // 2, dtype=torch.int16, device=dev)
-    d.fill_(3)
-    h = torch.empty(n // 2, dtype=torch.int16, pin_memory=True)
+    w = W.c4_llama70b_tp8()
+    sh = w.shape
+    R = w.num_reqs
+    s_all, e_all = w.starts[0], w.ends[0]
+    n_rows = w.step_tokens(0)
+    rb = sh.token_row_bytes
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+    pool = torch.empty(sh.pool_elems(w.num_blocks), dtype=torch.bfloat16,
+                       device=dev)
+    pool.normal_(generator=g)
+    arena = torch.empty(n_rows * sh.token_row_elems, dtype=torch.bfloat16,
+                        device=dev)
+    bt = torch.from_numpy(w.block_tables).to(dev)
+    bounds = np.linspace(0, R, chunks + 1).astype(int)
+    row_first = np.concatenate([[0], np.cumsum(e_all.astype(np.int64)
+                                              - s_all)])
+    wss, plans = [], []
+    for c in range(chunks):
+        r0, r1 = bounds[c], bounds[c + 1]
+        wss.append(kv.new_workspace(r1 - r0, dev))
+        plans.append((torch.from_numpy(s_all[r0:r1]).to(dev),
+                      torch.from_numpy(e_all[r0:r1]).to(dev),
+                      bt[r0:r1].contiguous(), int(row_first[r0])))
     side = torch.cuda.Stream()
-    kv.lumen_kv_ckpt_offload(d, h, side=side)
+    host = [torch.empty(slot_bytes // 2, dtype=torch.int16, pin_memory=True)
+            for _ in range(ring)]
+    slot_free = [None] * ring
+
+    def pack_all(events):
+        done = []
+        events[0].record()
+        for c, (s, e, btc, base) in enumerate(plans):
+            kv.lumen_kv_ckpt_plan(s, e, wss[c], base)
+            kv.lumen_kv_ckpt_pack(sh, w.num_blocks, pool, btc, wss[c], arena)
+            ev = torch.cuda.Event()
+            ev.record()
+            done.append(ev)
+        events[1].record()
+        return done
+
+    t_alone = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    pack_all(t_alone)
+    torch.cuda.synchronize()
+    for ws in wss:
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+    t_pack = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    d2h = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    done = pack_all(t_pack)
+    arena16 = arena.view(torch.int16)
+    piece = slot_bytes // 2
+    side.wait_event(done[0])
+    d2h[0].record(side)
+    nslot, checked = 0, []
+    for c in range(chunks):
+        lo = int(row_first[bounds[c]]) * rb // 2
+        hi = int(row_first[bounds[c + 1]]) * rb // 2
+        side.wait_event(done[c])
+        for off in range(lo, hi, piece):
+            j = nslot % ring
+            if slot_free[j] is not None:
+                slot_free[j].synchronize()  # the host drains the slot
+            n = min(piece, hi - off)
+            kv.lumen_kv_ckpt_offload(arena16[off:off + n], host[j],
+                                     nbytes=2 * n, producer=side, side=side)
+            ev = torch.cuda.Event()
+            ev.record(side)
+            slot_free[j] = ev
+            checked.append((off, n, j))
+            nslot += 1
+    d2h[1].record(side)
     side.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(3):
-        kv.lumen_kv_ckpt_offload(d, h, side=side)
-    side.synchronize()
-    dt = (time.perf_counter() - t0) / 3
-    ok = bool(h[:1024].eq(3).all())
-    return dict(d2h_GBps=gb(n) / dt, bytes=n, ok=ok)
+    torch.cuda.synchronize()
+    ok = True  # the last copy into each slot, against the device bytes
+    for off, n, j in checked[-ring:]:
+        k = min(n, 1 << 20)
+        ok &= bool(torch.equal(host[j][:k], arena16[off:off + k].cpu()))
+    for ws in wss:
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+    ws = kv.new_workspace(R, dev)
+    kv.lumen_kv_ckpt_plan(torch.from_numpy(s_all).to(dev),
+                          torch.from_numpy(e_all).to(dev), ws)
+    t_un = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    t_un[0].record()
+    kv.lumen_kv_ckpt_unpack(sh, w.num_blocks, pool,
+                            torch.from_numpy(w.dst_block_tables).to(dev), ws,
+                            arena)
+    t_un[1].record()
+    torch.cuda.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    byts = 2.0 * n_rows * rb
+    alone_ms = t_alone[0].elapsed_time(t_alone[1])
+    with_ms = t_pack[0].elapsed_time(t_pack[1])
+    un_ms = t_un[0].elapsed_time(t_un[1])
+    d2h_ms = d2h[0].elapsed_time(d2h[1])
+    del pool, arena, host
+    torch.cuda.empty_cache()
+    return dict(workload=w.name, requests=R, tokens=n_rows,
+                pack_GBps=gb(byts) / (alone_ms / 1e3), pack_ms=alone_ms,
+                pack_with_d2h_GBps=gb(byts) / (with_ms / 1e3),
+                pack_slowdown_with_d2h=with_ms / alone_ms,
+                unpack_in_place_GBps=gb(byts) / (un_ms / 1e3),
+                unpack_ms=un_ms,
+                d2h_GBps=gb(n_rows * rb) / (d2h_ms / 1e3), d2h_ms=d2h_ms,
+                d2h_bytes=n_rows * rb, d2h_spot_check_ok=ok,
+                pinned_ring=f"{ring} x {slot_bytes >> 30} GiB")
 
 
 def calibrate_copy(torch, mib):
@@ -298,13 +407,41 @@ def cpu_baseline(W, seconds):
 
 # -------------------------------------------------------------------- main
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles",
+                            "copy_rows_kernel_llama3-8b-decode_hbm_traffic.txt")
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_17787_amd", "csrc",
+                          "lumen_kv_ckpt.hip")
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed FETCH_SIZE /
+    WRITE_SIZE counter runs, or None once the kernel source has changed
+    since those counters were taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_FILE).read()
+        data = json.loads(text[text.index("{", text.index("Machine-readable")):])
+        sha = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None
+    if data.get("kernel_source_sha256") != sha:
+        return None
+    return data["llama3-8b-decode"][kernel]["traffic_bytes"]
+
+
+def rounded(d):
+    return {k: (round(v, 4) if isinstance(v, float) else v)
+            for k, v in d.items()}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the "
-              "checkpoint path has no cross-GPU exchange to measure",
-              file=sys.stderr)
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}): the "
+              "checkpoint path has no cross-GPU exchange; run it with "
+              "--gpus 1", file=sys.stderr)
         sys.exit(2)
+    legs = set(args.legs.split(","))
     import torch
     import paper_2606_17787_amd.kvckpt as kv
     from paper_2606_17787_amd import workloads as W
@@ -314,18 +451,18 @@ def main():
         return
     kv.load_library()
 
-    dec = decode_leg(torch, kv, W, args.steps, args.warmup)
-    w = dec.pop("workload")
-    ms_per_step = dec["wall_ms"] / dec["steps"]
-    value = gb(dec["bytes_total"]) / (dec["wall_ms"] / 1e3)
-    dominant = "pack" if dec["pack_us_mean"] >= dec["unpack_us_mean"] else "unpack"
+    say("[bench] decode leg (llama3-8b-decode)")
+    w = W.c2_llama8b()
+    dec = incremental_leg(torch, kv, w, args.steps, args.warmup, seed=2)
+    dominant = ("pack" if dec["pack_us_mean"] >= dec["unpack_us_mean"]
+                else "unpack")
     achieved = dec[f"{dominant}_GBps"]
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "GB/s",
+        "metric": METRIC, "value": round(dec["step_GBps"], 1), "unit": "GB/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic",
+        "ms_per_step": round(dec["ms_per_step"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.name, "layers": w.shape.num_layers,
                    "kv_heads": w.shape.num_kv_heads,
                    "head_dim": w.shape.head_dim,
@@ -336,25 +473,37 @@ def main():
                    "parallelism": "none (1 GPU)"},
         "pack_GBps": round(dec["pack_GBps"], 1),
         "unpack_GBps": round(dec["unpack_GBps"], 1),
-        "pack_pct_peak": round(100 * dec["pack_GBps"] / HBM_PEAK_GBPS, 2),
-        "unpack_pct_peak": round(100 * dec["unpack_GBps"] / HBM_PEAK_GBPS, 2),
-        "pack_us_median": round(dec["pack_us_median"], 2),
-        "unpack_us_median": round(dec["unpack_us_median"], 2),
+        "pack_pct_peak": round(dec["pack_pct_peak"], 2),
+        "unpack_pct_peak": round(dec["unpack_pct_peak"], 2),
+        "pack_us_mean": round(dec["pack_us_mean"], 2),
+        "unpack_us_mean": round(dec["unpack_us_mean"], 2),
         "roundtrip_ok": dec["roundtrip_ok"],
-        "roofline": {"bound": "hbm", "kernel": f"{dominant} (copy_rows_kernel)",
+        "roofline": {"bound": "hbm",
+                     "kernel": "copy_rows_kernel<%s, false> (%s)" % (
+                         "true" if dominant == "pack" else "false", dominant),
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "bytes_per_launch": dec[f"{dominant}_bytes_mean"],
-                     "traffic": None},
+                     "us_per_launch": round(dec[f"{dominant}_us_mean"], 2),
+                     "traffic": measured_traffic(dominant)},
+        "workloads": {},
     }
-    if not args.no_restore:
-        out["restore"] = restore_leg(torch, kv, W)
-        out["restore_ms_per_request"] = round(
-            out["restore"]["restore_ms_per_request"], 4)
-    if not args.no_offload:
-        out["offload"] = offload_leg(torch, kv)
-    if not args.no_cpu_baseline:
+    if "qwen" in legs:
+        say("[bench] decode leg (qwen-gqa-hnd)")
+        out["workloads"]["qwen-gqa-hnd"] = rounded(incremental_leg(
+            torch, kv, W.c5_qwen_hnd(), 64, 8, seed=5))
+    if "restore" in legs:
+        say("[bench] restore leg")
+        res = restore_leg(torch, kv, W)
+        out["restore_ms_per_request"] = round(res["restore_ms_per_request"], 4)
+        out["workloads"]["restore-burst"] = rounded(res)
+    if "tp8" in legs:
+        say("[bench] tp8-shard leg")
+        out["workloads"]["llama3-70b-tp8-shard"] = rounded(
+            tp8_leg(torch, kv, W))
+    if "cpu" in legs:
+        say("[bench] cpu baseline")
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

@@ -431,15 +431,20 @@ __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_
   }
 }
 
-// Row plan: one workgroup scans the per-request token counts.
+// Row plan: one workgroup scans the per-request token counts.  Each thread
+// sums a contiguous chunk of requests; the per-thread sums are scanned with
+// cross-lane shuffles inside each wavefront and once more across the
+// wavefronts' totals, so only two workgroup barriers are needed.
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t *__restrict__ d_start, const int32_t *__restrict__ d_end,
     int32_t R, int64_t row_base, const int64_t *__restrict__ req_row_base,
     WsHeader *hdr, int64_t *prefix, int64_t *first_row, int32_t *start) {
-  __shared__ int64_t scan[kPlanThreads];
+  constexpr int kWaves = kPlanThreads / kWave;
+  __shared__ int64_t wave_sum[kWaves];
   __shared__ int bad;
   const int tid = threadIdx.x;
-  if (tid == 0) bad = 0;
+  const int lane = tid & (kWave - 1);
+  const int wid = tid / kWave;
   const int32_t per = (R + kPlanThreads - 1) / kPlanThreads;
   const int32_t lo = min(R, tid * per);
   const int32_t hi = min(R, lo + per);
@@ -449,17 +454,28 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t s = d_start[i], e = d_end[i];
     if (s < 0 || e < s) my_bad = 1; else local += int64_t(e) - s;
   }
-  scan[tid] = local;
+  // Inclusive scan of the per-thread sums within the wavefront.
+  int64_t x = local;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t y = __shfl_up(x, d, kWave);
+    if (lane >= d) x += y;
+  }
+  if (lane == kWave - 1) wave_sum[wid] = x;
+  if (tid == 0) bad = 0;
   __syncthreads();
   if (my_bad) atomicOr(&bad, 1);
-  // Inclusive Hillis-Steele scan of the per-thread sums.
-  for (int off = 1; off < kPlanThreads; off <<= 1) {
-    const int64_t add = tid >= off ? scan[tid - off] : 0;
-    __syncthreads();
-    scan[tid] += add;
-    __syncthreads();
+  if (wid == 0) {  // inclusive scan of the wavefront totals
+    int64_t v = lane < kWaves ? wave_sum[lane] : 0;
+#pragma unroll
+    for (int d = 1; d < kWaves; d <<= 1) {
+      const int64_t y = __shfl_up(v, d, kWave);
+      if (lane >= d) v += y;
+    }
+    if (lane < kWaves) wave_sum[lane] = v;
   }
-  int64_t run = scan[tid] - local;  // exclusive
+  __syncthreads();
+  int64_t run = (wid > 0 ? wave_sum[wid - 1] : 0) + x - local;  // exclusive
   for (int32_t i = lo; i < hi; ++i) {
     const int32_t s = d_start[i], e = d_end[i];
     const bool ok = !(s < 0 || e < s);
@@ -469,13 +485,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     start[i] = ok ? s : 0;
     run += n;
   }
-  if (tid == kPlanThreads - 1) {
-    prefix[R] = scan[tid];
-    hdr->total_rows = scan[tid];
+  if (tid == 0) {
+    const int64_t total = wave_sum[kWaves - 1];
+    prefix[R] = total;
+    hdr->total_rows = total;
     hdr->num_reqs = R;
+    hdr->err = bad ? LUMEN_ERR_RANGE : LUMEN_OK;
   }
-  __syncthreads();
-  if (tid == 0) hdr->err = bad ? LUMEN_ERR_RANGE : LUMEN_OK;
 }
 
 // ------------------------------------------------------------- host side

@@ -228,3 +228,35 @@ def test_offload_and_stage_in_bytes():
     side.synchronize()
     got = host.numpy().view(np.uint16)
     assert np.array_equal(got[:500], a[:500]) and not got[500:].any()
+
+
+@pytest.mark.parametrize("R", [1, 63, 64, 65, 1023, 1024, 1025, 5000, 20001])
+def test_plan_many_requests(R):
+    """Plans over many requests (several per scan thread, partial
+    wavefronts), with empty and invalid ranges sprinkled in; the pack of
+    one-element rows checks every planned row against the oracle."""
+    shape = CacheShape(1, 1, 8, 4, NHD)
+    rng = np.random.default_rng(R)
+    cols = 3
+    nb = R * cols
+    bt = rng.permutation(nb).astype(np.int32).reshape(R, cols)
+    s = rng.integers(0, 12, R).astype(np.int32)
+    e = np.minimum(s + rng.integers(0, 5, R), 12).astype(np.int32)
+    empty = rng.random(R) < 0.1
+    e[empty] = s[empty]
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    disjoint = np.arange(R, dtype=np.int64) * 20 + rng.integers(0, 5, R)
+    for base, rb in ((0, None), (7, None), (0, disjoint)):
+        n = int((e - s).sum())
+        rows = n + base if rb is None else int(rb.max()) + 13
+        gpu = gpu_path(shape, nb, src, bt, s, e, row_base=base,
+                       req_row_base=rb, ckpt_rows=rows)
+        ref = oracle_path(shape, nb, src, bt, s, e, row_base=base,
+                          req_row_base=rb, ckpt_rows=rows)
+        assert_same(gpu, ref, f"R={R} base={base} per-request={rb is not None}")
+    # one invalid range: the plan reports RANGE and the rest still copies
+    if R > 1:
+        s2, e2 = s.copy(), e.copy()
+        s2[R // 2], e2[R // 2] = 5, 3
+        st, _, _ = gpu_path(shape, nb, src, bt, s2, e2)
+        assert st == kv.LUMEN_ERR_RANGE

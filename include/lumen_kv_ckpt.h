@@ -21,15 +21,16 @@
  *           rows on a side stream, ordered after (before) the main stream's
  *           work (the pinned CPU buffer of Sec. 4.2)
  *
- * Layouts.  The cache is one allocation of 16-bit elements (bf16, moved as
- * raw bits), layer-major, K before V:
+ * Layouts.  The cache is one allocation of elements of elem_bytes bytes
+ * (2 for bf16/fp16, 1 for an 8-bit cache, 4 for fp32; always moved as raw
+ * bits), layer-major, K before V:
  *   LUMEN_CACHE_NHD  [L][2][num_blocks][block_size][H][D]
  *   LUMEN_CACHE_HND  [L][2][num_blocks][H][block_size][D]
  * A block (page) holds block_size consecutive token positions of one request
  * (Sec. 2.1).  Block table row r, of bt_cols int32 entries, maps request r's
  * page j (tokens [j*block_size, (j+1)*block_size)) to a physical block.
  * A checkpoint row holds one token, all layers, K and V, token-major:
- *   row [L][2][H][D]   (row_bytes = L*2*H*D*2)
+ *   row [L][2][H][D]   (row_bytes = L*2*H*D*elem_bytes)
  * so the rows of successive increments append to a request's checkpoint and
  * any prefix of rows is a token prefix (the longest checkpointed prefix that
  * recovery restores, Sec. 4.3).
@@ -61,7 +62,11 @@ extern "C" {
 
 #define LUMEN_OK 0
 #define LUMEN_ERR_INVALID_ARG (-1) /* null pointer, negative size, bad dims */
-#define LUMEN_ERR_UNSUPPORTED (-2) /* elem_bytes != 2, unknown order, D*2 % 16 */
+#define LUMEN_ERR_UNSUPPORTED (-2) /* elem_bytes not 1/2/4, unknown order,
+                                      D*elem_bytes not a multiple of 16, a row
+                                      of 2^31 or more 16-byte vectors, or
+                                      H*D*elem_bytes or block_size*D*elem_bytes
+                                      of 2^31 bytes or more */
 #define LUMEN_ERR_MISALIGNED (-3)  /* cache/ckpt/workspace not 16-byte aligned */
 #define LUMEN_ERR_HIP (-4)         /* a HIP runtime call failed */
 #define LUMEN_ERR_RANGE (-5)       /* start < 0, end < start, or a page past bt_cols */
@@ -81,7 +86,7 @@ typedef struct lumen_kv_layout {
     int32_t head_dim;     /* D; D*elem_bytes must be a multiple of 16 */
     int32_t block_size;   /* tokens per block (page) */
     int64_t num_blocks;   /* blocks in the pool */
-    int32_t elem_bytes;   /* must be 2 (bf16/fp16, copied as raw bits) */
+    int32_t elem_bytes;   /* 1, 2 or 4 (fp8 / bf16 or fp16 / fp32; raw bits) */
     int32_t cache_order;  /* LUMEN_CACHE_NHD or LUMEN_CACHE_HND */
 } lumen_kv_layout;
 

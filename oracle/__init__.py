@@ -10,7 +10,7 @@ checkpoint pack gathers the token range [start, end) of every request out of
 the paged cache through its block table into token-major checkpoint rows
 (LUMEN Sec. 2.1 for pages, Sec. 4.2 for incremental ranges); unpack scatters
 checkpoint rows back into the blocks a new block table names (Sec. 4.3,
-KV-reuse recovery).  Element values are moved as raw 16-bit words.
+KV-reuse recovery).  Elements (1, 2 or 4 bytes) are moved as raw bits.
 """
 from __future__ import annotations
 
@@ -40,7 +40,15 @@ class _Shape(ctypes.Structure):
                 ("head_dim", ctypes.c_int32),
                 ("block_size", ctypes.c_int32),
                 ("num_blocks", ctypes.c_int64),
-                ("head_major", ctypes.c_int32)]
+                ("head_major", ctypes.c_int32),
+                ("elem_bytes", ctypes.c_int32)]
+
+_WORD = {1: np.uint8, 2: np.uint16, 4: np.uint32}
+
+
+def word_dtype(shape):
+    """Unsigned integer dtype of one cache element (raw bits)."""
+    return _WORD[getattr(shape, "elem_bytes", 2)]
 
 
 def build(src: str = _SRC, out: str = LIB_PATH, extra_flags=()) -> str:
@@ -94,7 +102,8 @@ def _i32(a) -> np.ndarray:
 def _shape(shape, num_blocks: int) -> _Shape:
     return _Shape(shape.num_layers, shape.num_kv_heads, shape.head_dim,
                   shape.block_size, int(num_blocks),
-                  1 if shape.order == "HND" else 0)
+                  1 if shape.order == "HND" else 0,
+                  getattr(shape, "elem_bytes", 2))
 
 
 def plan(start, end, row_base: int = 0, req_row_base=None,
@@ -116,9 +125,11 @@ def pack(shape, num_blocks: int, cache: np.ndarray, block_tables, start, end,
          ckpt_rows: Optional[int] = None,
          lib: Optional[ctypes.CDLL] = None) -> Tuple[int, np.ndarray]:
     """Gather the ranges into checkpoint rows.  `cache` is the flat pool as
-    uint16 words; returns (status, ckpt) with ckpt of shape [rows, row_elems]."""
+    raw element words; returns (status, ckpt) with ckpt of shape
+    [rows, row_elems] in the same word type."""
     lib = lib or load()
-    cache = np.ascontiguousarray(cache).view(np.uint16).reshape(-1)
+    word = word_dtype(shape)
+    cache = np.ascontiguousarray(cache).view(word).reshape(-1)
     assert cache.size == shape.pool_elems(num_blocks)
     bt = _i32(block_tables)
     assert bt.ndim == 2
@@ -130,9 +141,9 @@ def pack(shape, num_blocks: int, cache: np.ndarray, block_tables, start, end,
         if ckpt_rows is None:
             ckpt_rows = int(np.maximum(e.astype(np.int64) - s, 0).sum()) + \
                 max(int(row_base), 0)
-        ckpt = np.zeros((ckpt_rows, row_elems), np.uint16)
+        ckpt = np.zeros((ckpt_rows, row_elems), word)
     else:
-        assert ckpt.dtype == np.uint16 and ckpt.flags.c_contiguous
+        assert ckpt.dtype == word and ckpt.flags.c_contiguous
         ckpt_rows = ckpt.size // row_elems if ckpt_rows is None else ckpt_rows
         assert ckpt_rows * row_elems <= ckpt.size
     sh = _shape(shape, num_blocks)
@@ -147,17 +158,18 @@ def unpack(shape, num_blocks: int, cache: np.ndarray, block_tables, start,
            end, ckpt: np.ndarray, row_base: int = 0, req_row_base=None,
            ckpt_rows: Optional[int] = None,
            lib: Optional[ctypes.CDLL] = None) -> int:
-    """Scatter checkpoint rows into `cache` (a contiguous uint16 array that
-    is modified in place).  Returns the status."""
+    """Scatter checkpoint rows into `cache` (a contiguous array of element
+    words that is modified in place).  Returns the status."""
     lib = lib or load()
-    assert cache.dtype == np.uint16 and cache.flags.c_contiguous
+    word = word_dtype(shape)
+    assert cache.dtype == word and cache.flags.c_contiguous
     assert cache.size == shape.pool_elems(num_blocks)
     bt = _i32(block_tables)
     assert bt.ndim == 2
     s, e = _i32(start), _i32(end)
     base = (None if req_row_base is None else
             np.ascontiguousarray(np.asarray(req_row_base, np.int64)))
-    ck = np.ascontiguousarray(ckpt).view(np.uint16)
+    ck = np.ascontiguousarray(ckpt).view(word)
     row_elems = shape.token_row_elems
     if ckpt_rows is None:
         ckpt_rows = ck.size // row_elems

@@ -8,6 +8,7 @@
 #include "lumen_oracle.h"
 
 #include <stdlib.h>
+#include <string.h>
 
 /* Element offset of (layer l, k-or-v kv, block b, slot s, head h, dim d) in
  * the paged cache (Sec. 2.1: a page holds consecutive token positions). */
@@ -69,6 +70,8 @@ static int check_shape(const oracle_cache_shape *sh)
         return ORACLE_ERR_INVALID_ARG;
     if (sh->head_major != 0 && sh->head_major != 1)
         return ORACLE_ERR_UNSUPPORTED;
+    if (sh->elem_bytes != 1 && sh->elem_bytes != 2 && sh->elem_bytes != 4)
+        return ORACLE_ERR_UNSUPPORTED;
     return ORACLE_OK;
 }
 
@@ -123,10 +126,18 @@ static int prepare(const oracle_cache_shape *sh, const void *cache,
     return st;
 }
 
-int oracle_pack(const oracle_cache_shape *sh, const uint16_t *cache,
+/* Copies element `from` of `src` to element `to` of `dst`. */
+static void copy_elem(void *dst, int64_t to, const void *src, int64_t from,
+                      int32_t elem_bytes)
+{
+    memcpy((unsigned char *)dst + to * elem_bytes,
+           (const unsigned char *)src + from * elem_bytes, (size_t)elem_bytes);
+}
+
+int oracle_pack(const oracle_cache_shape *sh, const void *cache,
                 const int32_t *block_tables, int32_t bt_cols,
                 const int32_t *start, const int32_t *end, int32_t num_reqs,
-                int64_t row_base, const int64_t *req_row_base, uint16_t *ckpt,
+                int64_t row_base, const int64_t *req_row_base, void *ckpt,
                 int64_t ckpt_rows)
 {
     int64_t *first_row = malloc(sizeof(int64_t) * (num_reqs > 0 ? num_reqs : 1));
@@ -147,19 +158,20 @@ int oracle_pack(const oracle_cache_shape *sh, const uint16_t *cache,
                 for (int64_t kv = 0; kv < 2; ++kv)
                     for (int64_t h = 0; h < sh->num_kv_heads; ++h)
                         for (int64_t d = 0; d < sh->head_dim; ++d)
-                            ckpt[ckpt_index(sh, row, l, kv, h, d)] =
-                                cache[cache_index(sh, l, kv, b, slot, h, d)];
+                            copy_elem(ckpt, ckpt_index(sh, row, l, kv, h, d),
+                                      cache, cache_index(sh, l, kv, b, slot, h, d),
+                                      sh->elem_bytes);
         }
     }
     free(first_row);
     return ORACLE_OK;
 }
 
-int oracle_unpack(const oracle_cache_shape *sh, uint16_t *cache,
+int oracle_unpack(const oracle_cache_shape *sh, void *cache,
                   const int32_t *block_tables, int32_t bt_cols,
                   const int32_t *start, const int32_t *end, int32_t num_reqs,
                   int64_t row_base, const int64_t *req_row_base,
-                  const uint16_t *ckpt, int64_t ckpt_rows)
+                  const void *ckpt, int64_t ckpt_rows)
 {
     int64_t *first_row = malloc(sizeof(int64_t) * (num_reqs > 0 ? num_reqs : 1));
     if (!first_row)
@@ -179,8 +191,9 @@ int oracle_unpack(const oracle_cache_shape *sh, uint16_t *cache,
                 for (int64_t kv = 0; kv < 2; ++kv)
                     for (int64_t h = 0; h < sh->num_kv_heads; ++h)
                         for (int64_t d = 0; d < sh->head_dim; ++d)
-                            cache[cache_index(sh, l, kv, b, slot, h, d)] =
-                                ckpt[ckpt_index(sh, row, l, kv, h, d)];
+                            copy_elem(cache, cache_index(sh, l, kv, b, slot, h, d),
+                                      ckpt, ckpt_index(sh, row, l, kv, h, d),
+                                      sh->elem_bytes);
         }
     }
     free(first_row);

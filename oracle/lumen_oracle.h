@@ -17,7 +17,8 @@
  *  - On recovery the checkpointed prefix is loaded back into GPU memory, into
  *    whatever blocks the new block table names (Sec. 4.3, KV-reuse recovery).
  *
- * Layouts (element = 16-bit word, moved as raw bits):
+ * Layouts (an element is elem_bytes bytes -- 1 for an 8-bit cache, 2 for
+ * bf16/fp16, 4 for fp32 -- moved as raw bits):
  *   token-major cache  [L][2][NB][block_size][H][D]
  *   head-major cache   [L][2][NB][H][block_size][D]
  *   checkpoint rows    [rows][L][2][H][D]      (index 0 of the "2" is K)
@@ -49,6 +50,7 @@ typedef struct {
     int32_t block_size;   /* tokens per page */
     int64_t num_blocks;   /* NB, blocks in the pool */
     int32_t head_major;   /* 0: [L][2][NB][bs][H][D], 1: [L][2][NB][H][bs][D] */
+    int32_t elem_bytes;   /* 1, 2 or 4 */
 } oracle_cache_shape;
 
 /* Row of each request's first checkpointed token.
@@ -67,19 +69,19 @@ int oracle_plan(const int32_t *start, const int32_t *end, int32_t num_reqs,
  * 0 <= block < num_blocks (BLOCK_ID), 0 <= row < ckpt_rows (CAPACITY).
  * The status is the most negative code over all requests and tokens; on any
  * error nothing is written. */
-int oracle_pack(const oracle_cache_shape *shape, const uint16_t *cache,
+int oracle_pack(const oracle_cache_shape *shape, const void *cache,
                 const int32_t *block_tables, int32_t bt_cols,
                 const int32_t *start, const int32_t *end, int32_t num_reqs,
                 int64_t row_base, const int64_t *req_row_base,
-                uint16_t *ckpt, int64_t ckpt_rows);
+                void *ckpt, int64_t ckpt_rows);
 
 /* Scatter: the inverse of oracle_pack under (possibly different) block
  * tables.  Only the slots of the named tokens are written. */
-int oracle_unpack(const oracle_cache_shape *shape, uint16_t *cache,
+int oracle_unpack(const oracle_cache_shape *shape, void *cache,
                   const int32_t *block_tables, int32_t bt_cols,
                   const int32_t *start, const int32_t *end, int32_t num_reqs,
                   int64_t row_base, const int64_t *req_row_base,
-                  const uint16_t *ckpt, int64_t ckpt_rows);
+                  const void *ckpt, int64_t ckpt_rows);
 
 #ifdef __cplusplus
 }

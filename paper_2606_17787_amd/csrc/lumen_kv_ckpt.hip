@@ -4,9 +4,10 @@
 // file holds the three kernels (row plan, gather, scatter) and the C ABI.
 //
 // Work decomposition.  A checkpoint is a sequence of token rows, each
-// [L][2][H][D] 16-bit elements.  The copy is split into units of
+// [L][2][H][D] elements of E bytes (E = 1, 2 or 4; the copy moves raw bits
+// and never looks at values).  The copy is split into units of
 // (token row, layer): one unit is the K and V of one token in one layer,
-// 2*H*D*2 bytes, contiguous on the checkpoint side.  Units are numbered in
+// 2*H*D*E bytes, contiguous on the checkpoint side.  Units are numbered in
 // checkpoint order, u = packed_row * L + layer, and a persistent grid of
 // wavefronts splits [0, total_units) into equal contiguous spans, so every
 // wavefront moves the same number of bytes whatever the mix of request
@@ -14,8 +15,8 @@
 // request, its block-table entry and the checkpoint row of each token are
 // wave-uniform and live in scalar registers; the 64 lanes then move the
 // token's units as 16-byte vectors.  On the checkpoint side those vectors
-// are one contiguous run; on the cache side they are runs of H*D*2 bytes
-// (token-major cache) or D*2 bytes (head-major cache), each a whole number
+// are one contiguous run; on the cache side they are runs of H*D*E bytes
+// (token-major cache) or D*E bytes (head-major cache), each a whole number
 // of 128-byte lines for the serving shapes, so every access is full-line and
 // no LDS staging is needed for the head-major transpose.
 
@@ -134,21 +135,21 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f) {
 
 // Geometry shared by the gather and the scatter.
 struct Geom {
-  int64_t slab_bytes;   // stride of one (layer, K/V) slab: NB*bs*H*D*2
-  int64_t block_bytes;  // stride of one block inside a slab: bs*H*D*2
-  int64_t row_bytes;    // one checkpoint row: L*2*H*D*2
+  int64_t slab_bytes;   // stride of one (layer, K/V) slab: NB*bs*H*D*E
+  int64_t block_bytes;  // stride of one block inside a slab: bs*H*D*E
+  int64_t row_bytes;    // one checkpoint row: L*2*H*D*E
   int64_t num_blocks;
   int64_t ckpt_rows;
   int32_t num_layers;
   int32_t block_size;
-  int32_t slot_bytes;   // stride of one slot: H*D*2 (NHD) or D*2 (HND)
-  int32_t head_bytes;   // HND: stride of one head, bs*D*2
-  int32_t unit_vecs;    // 16-byte vectors per (token, layer): 2*H*D*2/16
+  int32_t slot_bytes;   // stride of one slot: H*D*E (NHD) or D*E (HND)
+  int32_t head_bytes;   // HND: stride of one head, bs*D*E
+  int32_t unit_vecs;    // 16-byte vectors per (token, layer): 2*H*D*E/16
   int32_t bt_cols;
   int32_t num_reqs;
   FastDiv div_unit;     // by unit_vecs
-  FastDiv div_kv;       // by H*D*2/16, vectors of one (token, layer, K/V)
-  FastDiv div_head;     // by D*2/16, vectors of one head
+  FastDiv div_kv;       // by H*D*E/16, vectors of one (token, layer, K/V)
+  FastDiv div_head;     // by D*E/16, vectors of one head
   FastDiv div_bs;       // by block_size
 };
 
@@ -541,7 +542,8 @@ int check_layout(const lumen_kv_layout *lay) {
   if (lay->num_layers <= 0 || lay->num_kv_heads <= 0 || lay->head_dim <= 0 ||
       lay->block_size <= 0 || lay->num_blocks < 0)
     return LUMEN_ERR_INVALID_ARG;
-  if (lay->elem_bytes != 2) return LUMEN_ERR_UNSUPPORTED;
+  if (lay->elem_bytes != 1 && lay->elem_bytes != 2 && lay->elem_bytes != 4)
+    return LUMEN_ERR_UNSUPPORTED;
   if (lay->cache_order != LUMEN_CACHE_NHD && lay->cache_order != LUMEN_CACHE_HND)
     return LUMEN_ERR_UNSUPPORTED;
   if ((int64_t(lay->head_dim) * lay->elem_bytes) % 16 != 0)
@@ -550,6 +552,11 @@ int check_layout(const lumen_kv_layout *lay) {
   const int64_t row_bytes = int64_t(lay->num_layers) * 2 * lay->num_kv_heads *
                             lay->head_dim * lay->elem_bytes;
   if (row_bytes / 16 >= (int64_t(1) << 31)) return LUMEN_ERR_UNSUPPORTED;
+  // Slot and head strides are 32-bit.
+  const int64_t d_bytes = int64_t(lay->head_dim) * lay->elem_bytes;
+  if (d_bytes * lay->num_kv_heads >= (int64_t(1) << 31) ||
+      d_bytes * lay->block_size >= (int64_t(1) << 31))
+    return LUMEN_ERR_UNSUPPORTED;
   return LUMEN_OK;
 }
 

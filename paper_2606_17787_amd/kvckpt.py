@@ -128,9 +128,14 @@ def _row_elems(shape) -> int:
     return shape.num_layers * 2 * shape.num_kv_heads * shape.head_dim
 
 
+def _elem_bytes(shape) -> int:
+    return getattr(shape, "elem_bytes", 2)
+
+
 def _check_cache(shape, num_blocks: int, cache: torch.Tensor, what: str):
-    if cache.element_size() != 2:
-        raise ValueError(f"{what} must have 2-byte elements")
+    if cache.element_size() != _elem_bytes(shape):
+        raise ValueError(f"{what} must have {_elem_bytes(shape)}-byte "
+                         "elements")
     need = (shape.num_layers * 2 * int(num_blocks) * shape.block_size
             * shape.num_kv_heads * shape.head_dim)
     if cache.numel() != need:
@@ -191,8 +196,10 @@ def _copy(name: str, shape, num_blocks: int, cache: torch.Tensor,
     if workspace.numel() * workspace.element_size() < \
             lumen_kv_ckpt_plan_workspace_bytes(R):
         raise ValueError("workspace too small for this many requests")
-    if ckpt.element_size() != 2 or ckpt.numel() % _row_elems(shape):
-        raise ValueError("checkpoint must hold whole rows of 2-byte elements")
+    if (ckpt.element_size() != _elem_bytes(shape)
+            or ckpt.numel() % _row_elems(shape)):
+        raise ValueError("checkpoint must hold whole rows of "
+                         f"{_elem_bytes(shape)}-byte elements")
     rows = ckpt.numel() // _row_elems(shape)
     lay = layout(shape, num_blocks)
     f = getattr(load_library(), name)
@@ -207,7 +214,8 @@ def lumen_kv_ckpt_pack(shape, num_blocks: int, cache: torch.Tensor,
                        ckpt: torch.Tensor,
                        stream: Optional[torch.cuda.Stream] = None) -> None:
     """Gather the planned token ranges of `cache` into `ckpt` rows
-    ([rows, L*2*H*D] 2-byte elements; rows = ckpt.numel() // row_elems)."""
+    ([rows, L*2*H*D] elements of elem_bytes bytes; rows =
+    ckpt.numel() // row_elems)."""
     _copy("lumen_kv_ckpt_pack", shape, num_blocks, cache, block_tables,
           workspace, ckpt, stream)
 

@@ -327,6 +327,17 @@ def random_bits(rng: np.random.Generator, n: int) -> np.ndarray:
     return rng.integers(0, 1 << 16, n, dtype=np.uint16)
 
 
+_WORDS = {1: np.uint8, 2: np.uint16, 4: np.uint32}
+
+
+def random_words(rng: np.random.Generator, n: int,
+                 elem_bytes: int = 2) -> np.ndarray:
+    """n uniformly random bit patterns of elem_bytes bytes each (1: 8-bit
+    caches, 2: bf16/fp16, 4: fp32)."""
+    w = _WORDS[elem_bytes]
+    return rng.integers(0, np.iinfo(w).max, n, dtype=w, endpoint=True)
+
+
 def normal_bf16_bits(rng: np.random.Generator, n: int) -> np.ndarray:
     """n ~N(0,1) values rounded to bf16 (round to nearest even), as bits."""
     x = rng.standard_normal(n, dtype=np.float32).view(np.uint32)

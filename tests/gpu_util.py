@@ -9,21 +9,31 @@ import torch
 import oracle
 import paper_2606_17787_amd.kvckpt as kv
 
-SENTINEL = 0x5A5A
+SENTINEL = 0x5A
 
 
 def dev():
     return torch.device("cuda:0")
 
 
+_SIGNED = {np.dtype(np.uint16): np.int16, np.dtype(np.uint32): np.int32}
+_WORD = {1: np.uint8, 2: np.uint16, 4: np.uint32}
+
+
 def h2d(a: np.ndarray) -> torch.Tensor:
-    if a.dtype == np.uint16:
-        a = a.view(np.int16)
-    return torch.from_numpy(np.ascontiguousarray(a)).to(dev())
+    """Host array to a device tensor (unsigned words travel as signed)."""
+    a = np.ascontiguousarray(a)
+    if a.dtype in _SIGNED:
+        a = a.view(_SIGNED[a.dtype])
+    return torch.from_numpy(a).to(dev())
 
 
 def d2h16(t: torch.Tensor) -> np.ndarray:
     return t.cpu().numpy().view(np.uint16)
+
+
+def d2h_words(t: torch.Tensor, elem_bytes: int) -> np.ndarray:
+    return t.cpu().numpy().view(_WORD[elem_bytes])
 
 
 def gpu_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None, dst_pool=None,
@@ -38,7 +48,8 @@ def gpu_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None, dst_pool=None,
     if ckpt_rows is None:
         ckpt_rows = int(np.maximum(e.astype(np.int64) - s, 0).sum()) + row_base
     row_elems = shape.token_row_elems
-    ck_h = np.full(max(ckpt_rows, 0) * row_elems, SENTINEL, np.uint16)
+    eb = shape.elem_bytes
+    ck_h = np.full(max(ckpt_rows, 0) * row_elems, SENTINEL, _WORD[eb])
     ck = h2d(ck_h)
     ws = kv.new_workspace(R, dev())
     rb = None if req_row_base is None else h2d(np.asarray(req_row_base, np.int64))
@@ -52,8 +63,8 @@ def gpu_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None, dst_pool=None,
         kv.lumen_kv_ckpt_unpack(shape, nb_dst, dst,
                                 h2d(np.asarray(bt_dst, np.int32)), ws, ck)
     st = kv.lumen_kv_ckpt_status(ws)
-    return (st, d2h16(ck).reshape(-1, row_elems),
-            None if dst is None else d2h16(dst))
+    return (st, d2h_words(ck, eb).reshape(-1, row_elems),
+            None if dst is None else d2h_words(dst, eb))
 
 
 def oracle_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None,
@@ -63,7 +74,8 @@ def oracle_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None,
     e = np.asarray(e, np.int32)
     if ckpt_rows is None:
         ckpt_rows = int(np.maximum(e.astype(np.int64) - s, 0).sum()) + row_base
-    ck = np.full((ckpt_rows, shape.token_row_elems), SENTINEL, np.uint16)
+    ck = np.full((ckpt_rows, shape.token_row_elems), SENTINEL,
+                 _WORD[shape.elem_bytes])
     st, ck = oracle.pack(shape, nb_src, src_pool, bt, s, e, row_base,
                          req_row_base, ckpt=ck)
     dst = None

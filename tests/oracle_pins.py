@@ -55,11 +55,20 @@ def to_logical(flat: np.ndarray, shape: CacheShape, nb: int) -> np.ndarray:
     return flat.reshape(L, 2, nb, bs, H, D)
 
 
+def word(shape):
+    return oracle.word_dtype(shape)
+
+
+def sentinel(shape):
+    """A value no coordinate code takes: the word's maximum."""
+    return np.iinfo(word(shape)).max
+
+
 def coded_pool(shape: CacheShape, nb: int) -> np.ndarray:
     dims = logical_dims(shape, nb)
     n = math.prod(dims)
-    assert n < 0xFFFF, "coordinate codes must fit 16 bits"
-    return to_physical(np.arange(n, dtype=np.uint16).reshape(dims),
+    assert n < sentinel(shape), "coordinate codes must fit the element"
+    return to_physical(np.arange(n, dtype=word(shape)).reshape(dims),
                        shape.order)
 
 
@@ -72,12 +81,22 @@ def first_rows(start, end, row_base=0, req_row_base=None):
     return list(itertools.accumulate(n, initial=row_base))[:len(n)]
 
 
+def _signed(shape):
+    """torch has no unsigned 16/32-bit tensors: move the bits as signed."""
+    return {1: np.uint8, 2: np.int16, 4: np.int32}[shape.elem_bytes]
+
+
+def random_words(rng, shape, n):
+    w = word(shape)
+    return rng.integers(0, np.iinfo(w).max, n, dtype=w, endpoint=True)
+
+
 def torch_gather(shape: CacheShape, nb: int, flat: np.ndarray, bt, start,
                  end) -> np.ndarray:
     """Checkpoint rows by torch advanced indexing, in request order."""
     L, H, D, bs = (shape.num_layers, shape.num_kv_heads, shape.head_dim,
                    shape.block_size)
-    t = torch.from_numpy(flat.view(np.int16).copy())
+    t = torch.from_numpy(flat.view(_signed(shape)).copy())
     if shape.order == HND:
         view = t.view(L, 2, nb, H, bs, D).permute(2, 4, 0, 1, 3, 5)
     else:
@@ -87,28 +106,28 @@ def torch_gather(shape: CacheShape, nb: int, flat: np.ndarray, bt, start,
         tok = torch.arange(int(start[r]), int(end[r]))
         b = torch.from_numpy(np.asarray(bt[r], np.int64))[tok // bs]
         parts.append(view[b, tok % bs].reshape(len(tok), L * 2 * H * D))
-    out = torch.cat(parts) if parts else torch.zeros(0, L * 2 * H * D,
-                                                     dtype=torch.int16)
-    return out.numpy().view(np.uint16)
+    out = torch.cat(parts) if parts else torch.zeros(
+        0, L * 2 * H * D, dtype=torch.from_numpy(np.zeros(1, _signed(shape))).dtype)
+    return out.numpy().view(word(shape))
 
 
 def torch_scatter(shape: CacheShape, nb: int, flat: np.ndarray, bt, start,
                   end, ckpt: np.ndarray) -> np.ndarray:
     L, H, D, bs = (shape.num_layers, shape.num_kv_heads, shape.head_dim,
                    shape.block_size)
-    t = torch.from_numpy(flat.view(np.int16).copy())
+    t = torch.from_numpy(flat.view(_signed(shape)).copy())
     if shape.order == HND:
         view = t.view(L, 2, nb, H, bs, D).permute(2, 4, 0, 1, 3, 5)
     else:
         view = t.view(L, 2, nb, bs, H, D).permute(2, 3, 0, 1, 4, 5)
-    ck = torch.from_numpy(ckpt.view(np.int16).reshape(-1, L, 2, H, D))
+    ck = torch.from_numpy(ckpt.view(_signed(shape)).reshape(-1, L, 2, H, D))
     row = 0
     for r in range(len(start)):
         tok = torch.arange(int(start[r]), int(end[r]))
         b = torch.from_numpy(np.asarray(bt[r], np.int64))[tok // bs]
         view.index_put_((b, tok % bs), ck[row:row + len(tok)])
         row += len(tok)
-    return t.numpy().view(np.uint16)
+    return t.numpy().view(word(shape))
 
 
 def random_table(rng, R, cols, nb, fill_all=True):
@@ -147,7 +166,7 @@ def check_decoded_pack(shape, nb, bt, s, e, lib, row_base=0):
     pool = coded_pool(shape, nb)
     n = int(np.sum(np.asarray(e, np.int64) - np.asarray(s, np.int64)))
     rows = row_base + n + 1  # one spare row that must stay untouched
-    ck = np.full((rows, L * 2 * H * D), 0xFFFF, np.uint16)
+    ck = np.full((rows, L * 2 * H * D), sentinel(shape), word(shape))
     st, ck = oracle.pack(shape, nb, pool, bt, s, e, row_base, ckpt=ck,
                          lib=lib)
     assert st == oracle.OK, st
@@ -166,7 +185,7 @@ def check_decoded_pack(shape, nb, bt, s, e, lib, row_base=0):
             assert np.array_equal(l, li) and np.array_equal(kv, kvi)
             assert np.array_equal(h, hi) and np.array_equal(d, di)
             assert np.all(b == bt[r][t // bs]) and np.all(slot == t % bs)
-    assert np.all(ck[~touched] == 0xFFFF)
+    assert np.all(ck[~touched] == sentinel(shape))
 
 
 def check_decoded_unpack(shape, nb, bt, s, e, lib):
@@ -175,9 +194,9 @@ def check_decoded_unpack(shape, nb, bt, s, e, lib):
                    shape.block_size)
     n = int(np.sum(np.asarray(e, np.int64) - np.asarray(s, np.int64)))
     cdims = (n, L, 2, H, D)
-    assert math.prod(cdims) < 0xFFFF
-    ck = np.arange(math.prod(cdims), dtype=np.uint16).reshape(n, L * 2 * H * D)
-    pool = np.full(shape.pool_elems(nb), 0xFFFF, np.uint16)
+    assert math.prod(cdims) < sentinel(shape)
+    ck = np.arange(math.prod(cdims), dtype=word(shape)).reshape(n, L * 2 * H * D)
+    pool = np.full(shape.pool_elems(nb), sentinel(shape), word(shape))
     st = oracle.unpack(shape, nb, pool, bt, s, e, ck, lib=lib)
     assert st == oracle.OK, st
     lg = to_logical(pool, shape, nb)
@@ -196,12 +215,14 @@ def check_decoded_unpack(shape, nb, bt, s, e, lib):
             assert np.array_equal(l, li) and np.array_equal(kv, kvi)
             assert np.array_equal(h, hi) and np.array_equal(d, di)
     rest = lg.transpose(2, 3, 0, 1, 4, 5)[~named]
-    assert np.all(rest == 0xFFFF)
+    assert np.all(rest == sentinel(shape))
 
 
 TINY_SHAPES = [CacheShape(1, 1, 8, bs, o) for bs in (1, 2, 3) for o in (NHD, HND)] + \
     [CacheShape(2, 2, 8, 2, o) for o in (NHD, HND)] + \
-    [CacheShape(1, 2, 16, 4, o) for o in (NHD, HND)]
+    [CacheShape(1, 2, 16, 4, o) for o in (NHD, HND)] + \
+    [CacheShape(2, 3, 4, 3, o, elem_bytes=4) for o in (NHD, HND)] + \
+    [CacheShape(1, 1, 16, 1, o, elem_bytes=1) for o in (NHD, HND)]
 
 
 def pin_bruteforce_decode(lib, exhaustive=True):
@@ -245,7 +266,11 @@ def _random_case(rng, shape, R, nb, max_tok, incremental=False):
 
 MEDIUM_SHAPES = [CacheShape(3, 2, 16, 4, NHD), CacheShape(3, 2, 16, 4, HND),
                  CacheShape(2, 4, 8, 16, NHD), CacheShape(2, 4, 8, 16, HND),
-                 CacheShape(1, 3, 24, 5, NHD), CacheShape(1, 3, 24, 5, HND)]
+                 CacheShape(1, 3, 24, 5, NHD), CacheShape(1, 3, 24, 5, HND),
+                 CacheShape(2, 2, 32, 4, NHD, elem_bytes=1),
+                 CacheShape(2, 3, 32, 4, HND, elem_bytes=1),
+                 CacheShape(2, 2, 4, 4, NHD, elem_bytes=4),
+                 CacheShape(1, 3, 8, 5, HND, elem_bytes=4)]
 
 
 def pin_torch_indexing(lib):
@@ -254,13 +279,11 @@ def pin_torch_indexing(lib):
         for inc in (False, True):
             nb = 64
             bt, s, e = _random_case(rng, shape, 5, nb, 40, inc)
-            pool = rng.integers(0, 1 << 16, shape.pool_elems(nb),
-                                dtype=np.uint16)
+            pool = random_words(rng, shape, shape.pool_elems(nb))
             st, ck = oracle.pack(shape, nb, pool, bt, s, e, lib=lib)
             assert st == oracle.OK
             assert np.array_equal(ck, torch_gather(shape, nb, pool, bt, s, e))
-            dst = rng.integers(0, 1 << 16, shape.pool_elems(nb),
-                               dtype=np.uint16)
+            dst = random_words(rng, shape, shape.pool_elems(nb))
             bt2 = random_table(rng, *bt.shape, nb)
             want = torch_scatter(shape, nb, dst, bt2, s, e, ck)
             assert oracle.unpack(shape, nb, dst, bt2, s, e, ck,
@@ -274,7 +297,7 @@ def pin_invariants(lib):
         nb, R, max_tok = 96, 6, 60
         bs = shape.block_size
         bt, _, e_full = _random_case(rng, shape, R, nb, max_tok)
-        pool = rng.integers(0, 1 << 16, shape.pool_elems(nb), dtype=np.uint16)
+        pool = random_words(rng, shape, shape.pool_elems(nb))
         s_full = np.zeros(R, np.int32)
         st, full = oracle.pack(shape, nb, pool, bt, s_full, e_full, lib=lib)
         assert st == oracle.OK
@@ -285,7 +308,7 @@ def pin_invariants(lib):
         bounds = np.concatenate([np.zeros((R, 1), np.int64), cuts,
                                  e_full[:, None]], axis=1)
         stride = max_tok + 1
-        per_req = np.zeros((R * stride, shape.token_row_elems), np.uint16)
+        per_req = np.zeros((R * stride, shape.token_row_elems), word(shape))
         steps = []
         for k in range(3):
             s_k, e_k = bounds[:, k].astype(np.int32), bounds[:, k + 1].astype(np.int32)
@@ -312,7 +335,7 @@ def pin_invariants(lib):
         assert np.array_equal(np.concatenate(regrouped), full)
 
         # round trip into a fresh table; untouched bytes unchanged
-        dst0 = rng.integers(0, 1 << 16, shape.pool_elems(nb), dtype=np.uint16)
+        dst0 = random_words(rng, shape, shape.pool_elems(nb))
         bt2 = random_table(rng, R, bt.shape[1], nb)
         s2 = rng.integers(0, e_full + 1).astype(np.int32)
         st, ck = oracle.pack(shape, nb, pool, bt, s2, e_full, lib=lib)
@@ -333,7 +356,8 @@ def pin_invariants(lib):
         # the same logical values in the other layout give the same bytes
         other = CacheShape(shape.num_layers, shape.num_kv_heads,
                            shape.head_dim, bs,
-                           NHD if shape.order == HND else HND)
+                           NHD if shape.order == HND else HND,
+                           shape.elem_bytes)
         lg = to_logical(pool, shape, nb)
         st, ck_other = oracle.pack(other, nb, to_physical(lg, other.order), bt,
                                    s_full, e_full, lib=lib)

@@ -70,7 +70,12 @@ def test_copy_host_validation(lib, fn):
     assert call(lay=_layout(num_kv_heads=-1)) == kv.LUMEN_ERR_INVALID_ARG
     assert call(lay=_layout(block_size=0)) == kv.LUMEN_ERR_INVALID_ARG
     assert call(lay=_layout(num_blocks=-1)) == kv.LUMEN_ERR_INVALID_ARG
-    assert call(lay=_layout(elem_bytes=4)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(lay=_layout(elem_bytes=3)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(lay=_layout(elem_bytes=8)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(lay=_layout(elem_bytes=0)) == kv.LUMEN_ERR_UNSUPPORTED
+    # a head row must be whole 16-byte vectors: 8 one-byte elements are not
+    assert call(lay=_layout(elem_bytes=1, head_dim=8)) == \
+        kv.LUMEN_ERR_UNSUPPORTED
     assert call(lay=_layout(cache_order=2)) == kv.LUMEN_ERR_UNSUPPORTED
     assert call(lay=_layout(head_dim=4)) == kv.LUMEN_ERR_UNSUPPORTED
     assert call(lay=_layout(head_dim=12)) == kv.LUMEN_ERR_UNSUPPORTED

@@ -40,6 +40,15 @@ SHAPES = [
     CacheShape(2, 1, 128, 16, NHD), CacheShape(3, 4, 128, 16, HND),
     CacheShape(2, 4, 64, 32, NHD), CacheShape(3, 2, 128, 32, HND),
     CacheShape(4, 8, 128, 16, NHD), CacheShape(1, 3, 40, 5, HND),
+    # 8-bit and fp32 caches (still 16-byte head rows)
+    CacheShape(1, 1, 16, 1, NHD, elem_bytes=1),
+    CacheShape(2, 3, 32, 3, HND, elem_bytes=1),
+    CacheShape(3, 8, 128, 16, NHD, elem_bytes=1),
+    CacheShape(2, 2, 128, 16, HND, elem_bytes=1),
+    CacheShape(1, 1, 4, 1, NHD, elem_bytes=4),
+    CacheShape(2, 3, 12, 5, HND, elem_bytes=4),
+    CacheShape(3, 4, 128, 16, NHD, elem_bytes=4),
+    CacheShape(2, 2, 64, 32, HND, elem_bytes=4),
 ]
 
 
@@ -59,12 +68,12 @@ def _case(rng, shape, R, max_tok, incremental, nb_extra=7):
     s, e = s.astype(np.int32), e.astype(np.int32)
     empty = rng.random(R) < 0.15
     e[empty] = s[empty]
-    src = W.random_bits(rng, shape.pool_elems(nb))
-    dst = W.random_bits(rng, shape.pool_elems(nb))
+    src = W.random_words(rng, shape.pool_elems(nb), shape.elem_bytes)
+    dst = W.random_words(rng, shape.pool_elems(nb), shape.elem_bytes)
     return nb, bt, bt2, s, e, src, dst
 
 
-@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"L{s.num_layers}H{s.num_kv_heads}D{s.head_dim}bs{s.block_size}{s.order}")
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"L{s.num_layers}H{s.num_kv_heads}D{s.head_dim}bs{s.block_size}{s.order}e{s.elem_bytes}")
 @pytest.mark.parametrize("incremental", [False, True])
 def test_random_shapes(shape, incremental):
     rng = np.random.default_rng(zlib.crc32(f"{shape}{incremental}".encode()))

@@ -72,6 +72,8 @@ extern "C" {
 #define LUMEN_ERR_RANGE (-5)       /* start < 0, end < start, or a page past bt_cols */
 #define LUMEN_ERR_BLOCK_ID (-6)    /* block table entry outside [0, num_blocks) */
 #define LUMEN_ERR_CAPACITY (-7)    /* checkpoint row outside [0, ckpt_rows) */
+#define LUMEN_ERR_DUP_BLOCK (-8)   /* validate mode: a block named by two
+                                      pages that an unpack would write */
 
 #define LUMEN_CACHE_NHD 0
 #define LUMEN_CACHE_HND 1
@@ -128,12 +130,39 @@ int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
  * the inverse of lumen_kv_ckpt_pack under d_block_tables (usually freshly
  * allocated, fragmented blocks).  Writes only the slots of the planned
  * tokens; every other byte of d_cache is left untouched.  Two planned tokens
- * mapping to the same (block, slot) race; the allocator must not do that. */
+ * mapping to the same (block, slot) race; the allocator must not do that
+ * (lumen_kv_ckpt_validate_targets checks for it). */
 int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
                          const int32_t *d_block_tables, int32_t bt_cols,
                          int32_t num_reqs, void *d_workspace,
                          const void *d_ckpt, int64_t ckpt_rows,
                          lumen_stream_t stream);
+
+/* Bytes of the mark buffer lumen_kv_ckpt_validate_targets needs for a pool
+ * of num_blocks blocks: one bit per block, rounded up to 16 bytes.  Returns
+ * 0 if num_blocks < 0. */
+size_t lumen_kv_ckpt_marks_bytes(int64_t num_blocks);
+
+/* Validate mode of a restore.  Recovery loads pages into blocks that an
+ * allocator hands out, one owner per block (Sec. 4.3), so a physical block
+ * named by two pages that an unpack writes is a caller error; the unpack
+ * itself does not look for it.  Run after lumen_kv_ckpt_plan and before the
+ * unpack, with the same plan and table.  The pages an unpack writes are,
+ * for every request with a non-empty planned range [start, end), pages
+ * start/block_size through (end-1)/block_size.  Each is checked: page <
+ * bt_cols (RANGE); block id in [0, num_blocks) (BLOCK_ID); no block named by
+ * two such pages (DUP_BLOCK).  Results go to the workspace's error word like
+ * the copies' (most negative code wins; read with lumen_kv_ckpt_status).
+ * d_marks: caller-owned device scratch of marks_bytes >=
+ * lumen_kv_ckpt_marks_bytes(num_blocks) bytes, 16-byte aligned, cleared by
+ * this call (by a kernel, not a memset); it may be NULL only if num_blocks
+ * is 0.  Calls sharing d_marks must not be in flight at the same time.
+ * Nothing in the cache or the checkpoint is read or written. */
+int lumen_kv_ckpt_validate_targets(const lumen_kv_layout *layout,
+                                   const int32_t *d_block_tables,
+                                   int32_t bt_cols, int32_t num_reqs,
+                                   void *d_workspace, void *d_marks,
+                                   size_t marks_bytes, lumen_stream_t stream);
 
 /* Synchronises `stream`, then returns and clears the workspace's error word
  * (LUMEN_OK if no device-side error was recorded since the last plan). */

@@ -32,6 +32,7 @@ ERR_UNSUPPORTED = -2
 ERR_RANGE = -5
 ERR_BLOCK_ID = -6
 ERR_CAPACITY = -7
+ERR_DUP_BLOCK = -8
 
 
 class _Shape(ctypes.Structure):
@@ -69,6 +70,9 @@ def _bind(lib: ctypes.CDLL) -> ctypes.CDLL:
         f.restype = ctypes.c_int
         f.argtypes = [ctypes.POINTER(_Shape), p, p, i32, p, p, i32, i64, p,
                       p, i64]
+    lib.oracle_validate_targets.restype = ctypes.c_int
+    lib.oracle_validate_targets.argtypes = [ctypes.POINTER(_Shape), p, i32,
+                                            p, p, i32]
     return lib
 
 
@@ -179,3 +183,18 @@ def unpack(shape, num_blocks: int, cache: np.ndarray, block_tables, start,
                              bt.shape[1], _ptr(s),
                              _ptr(e), s.shape[0], int(row_base), _ptr(base),
                              _ptr(ck), int(ckpt_rows))
+
+
+def validate_targets(shape, num_blocks: int, block_tables, start, end,
+                     lib: Optional[ctypes.CDLL] = None) -> int:
+    """Status of the blocks an unpack of [start, end) under `block_tables`
+    would write: RANGE / BLOCK_ID for pages past the table or outside the
+    pool, DUP_BLOCK when one block is named by two written pages."""
+    lib = lib or load()
+    bt = _i32(block_tables)
+    assert bt.ndim == 2
+    s, e = _i32(start), _i32(end)
+    assert s.shape == e.shape and bt.shape[0] == s.shape[0]
+    sh = _shape(shape, num_blocks)
+    return lib.oracle_validate_targets(ctypes.byref(sh), _ptr(bt), bt.shape[1],
+                                       _ptr(s), _ptr(e), s.shape[0])

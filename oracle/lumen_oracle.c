@@ -199,3 +199,48 @@ int oracle_unpack(const oracle_cache_shape *sh, void *cache,
     free(first_row);
     return ORACLE_OK;
 }
+
+int oracle_validate_targets(const oracle_cache_shape *sh,
+                            const int32_t *block_tables, int32_t bt_cols,
+                            const int32_t *start, const int32_t *end,
+                            int32_t num_reqs)
+{
+    int status = check_shape(sh);
+    if (status != ORACLE_OK)
+        return status;
+    if (num_reqs < 0 || bt_cols < 0)
+        return ORACLE_ERR_INVALID_ARG;
+    if (num_reqs > 0 && (!block_tables || !start || !end))
+        return ORACLE_ERR_INVALID_ARG;
+    /* times[b]: how many written pages name block b */
+    int32_t *times = calloc((size_t)sh->num_blocks + 1, sizeof(int32_t));
+    if (!times)
+        return ORACLE_ERR_INVALID_ARG;
+    for (int32_t r = 0; r < num_reqs; ++r) {
+        if (start[r] < 0 || end[r] < start[r]) {
+            status = worse(status, ORACLE_ERR_RANGE);
+            continue;
+        }
+        if (end[r] == start[r])
+            continue;
+        int64_t first = start[r] / sh->block_size;
+        int64_t last = (end[r] - 1) / sh->block_size;
+        for (int64_t page = first; page <= last; ++page) {
+            if (page >= bt_cols) {
+                status = worse(status, ORACLE_ERR_RANGE);
+                continue;
+            }
+            int64_t b = block_tables[(int64_t)r * bt_cols + page];
+            if (b < 0 || b >= sh->num_blocks) {
+                status = worse(status, ORACLE_ERR_BLOCK_ID);
+                continue;
+            }
+            times[b] += 1;
+        }
+    }
+    for (int64_t b = 0; b < sh->num_blocks; ++b)
+        if (times[b] > 1)
+            status = worse(status, ORACLE_ERR_DUP_BLOCK);
+    free(times);
+    return status;
+}

@@ -42,6 +42,7 @@ extern "C" {
 #define ORACLE_ERR_RANGE (-5)
 #define ORACLE_ERR_BLOCK_ID (-6)
 #define ORACLE_ERR_CAPACITY (-7)
+#define ORACLE_ERR_DUP_BLOCK (-8)
 
 typedef struct {
     int32_t num_layers;   /* L */
@@ -82,6 +83,19 @@ int oracle_unpack(const oracle_cache_shape *shape, void *cache,
                   const int32_t *start, const int32_t *end, int32_t num_reqs,
                   int64_t row_base, const int64_t *req_row_base,
                   const void *ckpt, int64_t ckpt_rows);
+
+/* Validate mode of a restore.  Recovery loads pages into blocks that an
+ * allocator hands out, one owner per block (Sec. 4.3), so a physical block
+ * named by two written pages is a caller error.  The pages an unpack writes
+ * are, for each request with a valid non-empty range, pages start/bs through
+ * (end-1)/bs.  Each is checked: page < bt_cols (RANGE), block in the pool
+ * (BLOCK_ID), and no block named by two such pages (DUP_BLOCK).  An invalid
+ * range (start < 0 or end < start) is a RANGE error, as in oracle_plan.
+ * Returns the most negative code found. */
+int oracle_validate_targets(const oracle_cache_shape *shape,
+                            const int32_t *block_tables, int32_t bt_cols,
+                            const int32_t *start, const int32_t *end,
+                            int32_t num_reqs);
 
 #ifdef __cplusplus
 }

@@ -495,6 +495,53 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
 }
 
+// Validate mode, step 1: clear the mark bits (a kernel rather than a memset,
+// so that the call can be captured in a graph).
+__global__ __launch_bounds__(kBlockThreads) void clear_marks_kernel(
+    uint4 *__restrict__ marks, int64_t n16) {
+  const int64_t stride = int64_t(gridDim.x) * kBlockThreads;
+  for (int64_t i = int64_t(blockIdx.x) * kBlockThreads + threadIdx.x; i < n16;
+       i += stride)
+    marks[i] = make_uint4(0, 0, 0, 0);
+}
+
+// Validate mode, step 2: one workgroup per request (grid-strided) walks the
+// pages the unpack of its planned range writes, pages start/bs through
+// (end-1)/bs, and sets one mark bit per physical block.  The atomic OR
+// returns the previous word, so of two pages naming one block exactly one
+// sees the bit already set, whatever the order.
+__global__ __launch_bounds__(kBlockThreads) void validate_kernel(
+    const int32_t *__restrict__ block_tables, const WsHeader *__restrict__ hdr,
+    const int64_t *__restrict__ prefix, const int32_t *__restrict__ start,
+    uint32_t *marks, int32_t *err, int32_t num_reqs, int32_t bt_cols,
+    int32_t block_size, int64_t num_blocks) {
+  if (hdr->num_reqs != num_reqs) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) atomicMin(err, LUMEN_ERR_INVALID_ARG);
+    return;
+  }
+  for (int32_t r = blockIdx.x; r < num_reqs; r += gridDim.x) {
+    const int64_t n = prefix[r + 1] - prefix[r];
+    if (n == 0) continue;
+    const int64_t s = start[r];
+    const int64_t first = s / block_size, last = (s + n - 1) / block_size;
+    for (int64_t j = first + threadIdx.x; j <= last; j += kBlockThreads) {
+      int code = LUMEN_OK;
+      if (j >= bt_cols) {
+        code = LUMEN_ERR_RANGE;
+      } else {
+        const int32_t b = block_tables[int64_t(r) * bt_cols + j];
+        if (b < 0 || b >= num_blocks) {
+          code = LUMEN_ERR_BLOCK_ID;
+        } else {
+          const uint32_t bit = 1u << (b & 31);
+          if (atomicOr(&marks[b >> 5], bit) & bit) code = LUMEN_ERR_DUP_BLOCK;
+        }
+      }
+      if (code != LUMEN_OK) atomicMin(err, code);
+    }
+  }
+}
+
 // ------------------------------------------------------------- host side
 
 constexpr int kMaxDevices = 64;
@@ -679,6 +726,48 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
                      num_reqs, d_workspace, ckpt_rows, stream);
 }
 
+size_t lumen_kv_ckpt_marks_bytes(int64_t num_blocks) {
+  if (num_blocks < 0) return 0;
+  return size_t((num_blocks + 127) / 128) * 16;
+}
+
+int lumen_kv_ckpt_validate_targets(const lumen_kv_layout *layout,
+                                   const int32_t *d_block_tables,
+                                   int32_t bt_cols, int32_t num_reqs,
+                                   void *d_workspace, void *d_marks,
+                                   size_t marks_bytes, lumen_stream_t stream) {
+  int st = check_layout(layout);
+  if (st != LUMEN_OK) return st;
+  if (num_reqs < 0 || bt_cols < 0 || !d_workspace) return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(d_workspace) || !aligned16(d_marks)) return LUMEN_ERR_MISALIGNED;
+  if (num_reqs == 0) return LUMEN_OK;
+  const size_t need = lumen_kv_ckpt_marks_bytes(layout->num_blocks);
+  if (marks_bytes < need || (!d_marks && need > 0) ||
+      (!d_block_tables && bt_cols > 0))
+    return LUMEN_ERR_INVALID_ARG;
+  DeviceInfo *dev = nullptr;
+  st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  WsView v = ws_view(d_workspace, num_reqs);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t n16 = int64_t(need / 16);
+  if (n16 > 0) {
+    const int64_t cap = int64_t(dev->cus) * 4;
+    int64_t blocks = (n16 + kBlockThreads - 1) / kBlockThreads;
+    if (blocks > cap) blocks = cap;
+    hipLaunchKernelGGL(clear_marks_kernel, dim3(unsigned(blocks)),
+                       dim3(kBlockThreads), 0, s,
+                       static_cast<uint4 *>(d_marks), n16);
+  }
+  const int32_t blocks = num_reqs < 65536 ? num_reqs : 65536;
+  hipLaunchKernelGGL(validate_kernel, dim3(unsigned(blocks)),
+                     dim3(kBlockThreads), 0, s, d_block_tables, v.hdr,
+                     v.prefix, v.start, static_cast<uint32_t *>(d_marks),
+                     &v.hdr->err, num_reqs, bt_cols, layout->block_size,
+                     layout->num_blocks);
+  return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
+}
+
 int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream) {
   if (!d_workspace) return LUMEN_ERR_INVALID_ARG;
   if (!aligned16(d_workspace)) return LUMEN_ERR_MISALIGNED;
@@ -706,6 +795,7 @@ const char *lumen_kv_ckpt_strerror(int code) {
     case LUMEN_ERR_RANGE: return "token range outside the request or its block table";
     case LUMEN_ERR_BLOCK_ID: return "block table entry outside the pool";
     case LUMEN_ERR_CAPACITY: return "checkpoint row outside the checkpoint buffer";
+    case LUMEN_ERR_DUP_BLOCK: return "block named by two pages of an unpack";
     default: return "unknown status";
   }
 }

@@ -33,6 +33,7 @@ LUMEN_ERR_HIP = -4
 LUMEN_ERR_RANGE = -5
 LUMEN_ERR_BLOCK_ID = -6
 LUMEN_ERR_CAPACITY = -7
+LUMEN_ERR_DUP_BLOCK = -8
 LUMEN_CACHE_NHD = 0
 LUMEN_CACHE_HND = 1
 
@@ -81,6 +82,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_pack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
         "lumen_kv_ckpt_unpack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
         "lumen_kv_ckpt_status": (ctypes.c_int, [p, p]),
+        "lumen_kv_ckpt_marks_bytes": (sz, [i64]),
+        "lumen_kv_ckpt_validate_targets": (ctypes.c_int,
+                                           [lay, p, i32, i32, p, p, sz, p]),
         "lumen_kv_ckpt_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         "lumen_kv_ckpt_offload": (ctypes.c_int, [p, p, sz, p, p]),
         "lumen_kv_ckpt_stage_in": (ctypes.c_int, [p, p, sz, p, p]),
@@ -227,6 +231,42 @@ def lumen_kv_ckpt_unpack(shape, num_blocks: int, cache: torch.Tensor,
     """Scatter the planned checkpoint rows of `ckpt` into `cache`."""
     _copy("lumen_kv_ckpt_unpack", shape, num_blocks, cache, block_tables,
           workspace, ckpt, stream)
+
+
+def lumen_kv_ckpt_marks_bytes(num_blocks: int) -> int:
+    return int(load_library().lumen_kv_ckpt_marks_bytes(int(num_blocks)))
+
+
+def new_marks(num_blocks: int, device=None) -> torch.Tensor:
+    """Device scratch for lumen_kv_ckpt_validate_targets over a pool of
+    num_blocks blocks."""
+    n = lumen_kv_ckpt_marks_bytes(num_blocks)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=device or "cuda")
+
+
+def lumen_kv_ckpt_validate_targets(shape, num_blocks: int,
+                                   block_tables: torch.Tensor,
+                                   workspace: torch.Tensor,
+                                   marks: torch.Tensor,
+                                   stream: Optional[torch.cuda.Stream] = None
+                                   ) -> None:
+    """Validate mode of a restore: records RANGE / BLOCK_ID / DUP_BLOCK in
+    the workspace's error word for the pages an unpack under this plan and
+    table would write (read it with lumen_kv_ckpt_status)."""
+    R = block_tables.shape[0] if block_tables.dim() == 2 else -1
+    _check_tables(block_tables, R)
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    nbytes = _nbytes(marks)
+    if nbytes < lumen_kv_ckpt_marks_bytes(num_blocks):
+        raise ValueError("marks buffer too small for this pool")
+    lay = layout(shape, num_blocks)
+    _check(load_library().lumen_kv_ckpt_validate_targets(
+        ctypes.byref(lay), _dev(block_tables, "block_tables", torch.int32),
+        block_tables.shape[1], R, _dev(workspace, "workspace"),
+        _dev(marks, "marks"), nbytes, _stream_handle(stream)),
+        "lumen_kv_ckpt_validate_targets")
 
 
 def lumen_kv_ckpt_status(workspace: torch.Tensor,

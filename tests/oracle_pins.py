@@ -415,5 +415,89 @@ def pin_error_codes(lib):
     assert st_pack([40, 3], [40, 3]) == oracle.OK
 
 
+def validate_by_tokens(bs, nb, bt, start, end):
+    """Validate-mode status written from its definition, token by token: a
+    request's written pages are the pages of its tokens; a physical block
+    named by two distinct (request, page) pairs is a duplicate."""
+    codes = [oracle.OK]
+    pages = set()
+    for r, (s, e) in enumerate(zip(start, end)):
+        if s < 0 or e < s:
+            codes.append(oracle.ERR_RANGE)
+            continue
+        for t in range(s, e):
+            j = t // bs
+            if j >= len(bt[r]):
+                codes.append(oracle.ERR_RANGE)
+            elif not 0 <= bt[r][j] < nb:
+                codes.append(oracle.ERR_BLOCK_ID)
+            else:
+                pages.add((r, j))
+    for x, y in itertools.combinations(sorted(pages), 2):
+        if bt[x[0]][x[1]] == bt[y[0]][y[1]]:
+            codes.append(oracle.ERR_DUP_BLOCK)
+    return min(codes)
+
+
+def pin_validate_targets(lib, exhaustive=True):
+    # every 2x2 table over entries {-1..3} with a pool of 3 blocks (entry 3
+    # is outside it), against sampled ranges, for three block sizes
+    nb, R, cols = 3, 2, 2
+    rng = np.random.default_rng(23)
+    for bs in (1, 2, 3):
+        shape = CacheShape(1, 1, 8, bs, NHD)
+        cap = cols * bs
+        spans = [(s, e) for s in range(cap + 2) for e in range(s, cap + 2)]
+        spans += [(-1, 2), (2, 1)]
+        tables = list(itertools.product(range(-1, 4), repeat=R * cols))
+        if not exhaustive:
+            tables = [tables[i] for i in rng.choice(len(tables), 60, False)]
+        for flat in tables:
+            bt = np.array(flat, np.int32).reshape(R, cols)
+            for _ in range(6):
+                (s0, e0), (s1, e1) = (spans[i] for i in
+                                      rng.choice(len(spans), 2))
+                want = validate_by_tokens(bs, nb, bt.tolist(), [s0, s1],
+                                          [e0, e1])
+                got = oracle.validate_targets(shape, nb, bt, [s0, s1],
+                                              [e0, e1], lib=lib)
+                assert got == want, (bs, flat, (s0, e0, s1, e1), got, want)
+    # larger cases: injective tables validate; one planted duplicate among
+    # the written pages is caught, one among unwritten pages is not; and
+    # whenever validation passes, unpack then pack round-trips
+    for shape in MEDIUM_SHAPES[:4]:
+        for trial in range(6):
+            R, nb, max_tok = 9, 90, 37
+            bt, s, e = _random_case(rng, shape, R, nb, max_tok,
+                                    incremental=trial % 2 == 1)
+            bs = shape.block_size
+            assert oracle.validate_targets(shape, nb, bt, s, e,
+                                           lib=lib) == oracle.OK
+            written = [(r, j) for r in range(R) if e[r] > s[r]
+                       for j in range(s[r] // bs, (e[r] - 1) // bs + 1)]
+            unwritten = [(r, j) for r in range(R) for j in range(bt.shape[1])
+                         if (r, j) not in set(written) and bt[r, j] >= 0]
+            ck = random_words(rng, shape,
+                              int((e - s).sum()) * shape.token_row_elems)
+            pool = random_words(rng, shape, shape.pool_elems(nb))
+            assert oracle.unpack(shape, nb, pool, bt, s, e, ck,
+                                 lib=lib) == oracle.OK
+            st, back = oracle.pack(shape, nb, pool, bt, s, e, lib=lib)
+            assert st == oracle.OK and np.array_equal(back.reshape(-1), ck)
+            if len(written) >= 2:
+                a, b = (written[i] for i in rng.choice(len(written), 2, False))
+                dup = bt.copy()
+                dup[b] = dup[a]
+                assert oracle.validate_targets(shape, nb, dup, s, e,
+                                               lib=lib) == oracle.ERR_DUP_BLOCK
+            if written and unwritten:
+                a = written[rng.integers(len(written))]
+                b = unwritten[rng.integers(len(unwritten))]
+                dup = bt.copy()
+                dup[b] = dup[a]
+                assert oracle.validate_targets(shape, nb, dup, s, e,
+                                               lib=lib) == oracle.OK
+
+
 ALL_PINS = [pin_plan_prefix_sum, pin_bruteforce_decode, pin_torch_indexing,
-            pin_invariants, pin_error_codes]
+            pin_invariants, pin_error_codes, pin_validate_targets]

@@ -22,7 +22,9 @@ def test_exports_every_declared_entry_point(lib):
                           "lumen_kv_ckpt_unpack", "lumen_kv_ckpt_status",
                           "lumen_kv_ckpt_strerror",
                           "lumen_kv_ckpt_plan_workspace_bytes",
-                          "lumen_kv_ckpt_offload", "lumen_kv_ckpt_stage_in"}
+                          "lumen_kv_ckpt_offload", "lumen_kv_ckpt_stage_in",
+                          "lumen_kv_ckpt_marks_bytes",
+                          "lumen_kv_ckpt_validate_targets"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -33,7 +35,7 @@ def test_missing_library_fails_loudly(tmp_path):
 
 
 def test_strerror(lib):
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         assert kv.lumen_kv_ckpt_strerror(code) not in ("", "unknown status")
     assert kv.lumen_kv_ckpt_strerror(-99) == "unknown status"
 
@@ -95,6 +97,41 @@ def test_copy_host_validation(lib, fn):
     assert call(bt=None, cols=0) in (kv.LUMEN_OK, kv.LUMEN_ERR_HIP)
     assert call(cache=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
     assert call(ck=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+
+
+def test_marks_bytes():
+    assert kv.lumen_kv_ckpt_marks_bytes(-1) == 0
+    assert kv.lumen_kv_ckpt_marks_bytes(0) == 0
+    for nb in (1, 127, 128, 129, 56323, 182657):
+        n = kv.lumen_kv_ckpt_marks_bytes(nb)
+        assert n % 16 == 0 and n * 8 >= nb and (n - 16) * 8 < nb
+
+
+def test_validate_targets_host_validation(lib):
+    f = lib.lumen_kv_ckpt_validate_targets
+    need = kv.lumen_kv_ckpt_marks_bytes(8)
+
+    def call(lay=None, bt=FAKE, cols=4, R=2, ws=FAKE, marks=FAKE,
+             nbytes=need):
+        lay = _layout() if lay is None else lay
+        return f(ctypes.byref(lay) if lay is not False else None, bt, cols, R,
+                 ws, marks, nbytes, None)
+
+    assert call(lay=False) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(block_size=0)) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(elem_bytes=3)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(R=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(cols=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ws=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ws=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+    assert call(marks=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+    assert call(nbytes=need - 1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(marks=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(bt=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(R=0, bt=None, marks=None, nbytes=0) == kv.LUMEN_OK
+    # an empty pool needs no marks (passes on to the first HIP call)
+    assert call(lay=_layout(num_blocks=0), marks=None, nbytes=0) in (
+        kv.LUMEN_OK, kv.LUMEN_ERR_HIP)
 
 
 def test_plan_host_validation(lib):

@@ -269,3 +269,99 @@ def test_plan_many_requests(R):
         s2[R // 2], e2[R // 2] = 5, 3
         st, _, _ = gpu_path(shape, nb, src, bt, s2, e2)
         assert st == kv.LUMEN_ERR_RANGE
+
+
+def gpu_validate(shape, nb, bt, s, e, marks=None):
+    """Plan + validate on the GPU; returns the status word."""
+    s = np.asarray(s, np.int32)
+    e = np.asarray(e, np.int32)
+    ws = kv.new_workspace(s.shape[0], dev())
+    kv.lumen_kv_ckpt_plan(h2d(s), h2d(e), ws)
+    marks = kv.new_marks(nb, dev()) if marks is None else marks
+    kv.lumen_kv_ckpt_validate_targets(shape, nb,
+                                      h2d(np.asarray(bt, np.int32)), ws, marks)
+    return kv.lumen_kv_ckpt_status(ws)
+
+
+def _written_pages(bt, s, e, bs):
+    return [(r, j) for r in range(bt.shape[0]) if 0 <= s[r] < e[r]
+            for j in range(s[r] // bs, (e[r] - 1) // bs + 1)
+            if j < bt.shape[1]]
+
+
+@pytest.mark.parametrize("shape", SHAPES[:6], ids=lambda s: f"bs{s.block_size}{s.order}")
+def test_validate_targets_matches_oracle(shape):
+    rng = np.random.default_rng(zlib.crc32(f"validate{shape}".encode()))
+    bs = shape.block_size
+    for R, max_tok in ((1, 7), (5, 40), (33, 100)):
+        nb, bt, _, s, e, _, _ = _case(rng, shape, R, max_tok, True)
+        variants = [("clean", bt, s, e)]
+        pages = _written_pages(bt, s, e, bs)
+        if len(pages) >= 2:
+            a, b = (pages[i] for i in rng.choice(len(pages), 2, False))
+            dup = bt.copy()
+            dup[b] = dup[a]
+            variants.append(("dup written", dup, s, e))
+        if pages:
+            unwritten = [(r, j) for r in range(R) for j in range(bt.shape[1])
+                         if (r, j) not in set(pages)]
+            if unwritten:
+                dup = bt.copy()
+                dup[unwritten[0]] = dup[pages[0]]
+                variants.append(("dup unwritten", dup, s, e))
+            bad = bt.copy()
+            bad[pages[-1]] = nb
+            variants.append(("outside pool", bad, s, e))
+            neg = bt.copy()
+            neg[pages[0]] = -1
+            variants.append(("padding entry", neg, s, e))
+        past_e = e.copy()
+        past_e[0] = bt.shape[1] * bs + 3
+        variants.append(("past table", bt, s, past_e))
+        inv_s = s.copy()
+        inv_s[-1] = -2
+        variants.append(("negative start", bt, inv_s, e))
+        for what, t, ss, ee in variants:
+            want = oracle.validate_targets(shape, nb, t, ss, ee)
+            got = gpu_validate(shape, nb, t, ss, ee)
+            assert got == want, (what, R, got, want)
+
+
+def test_validate_reuses_marks_and_strides_over_requests():
+    """70000 one-page requests (more than one grid's worth of workgroups);
+    the same marks buffer serves a call with a duplicate and then a clean
+    call, so stale bits from the first must not leak into the second."""
+    shape = CacheShape(1, 1, 8, 4, NHD)
+    R = 70000
+    rng = np.random.default_rng(77)
+    nb = R + 5
+    bt = rng.permutation(nb)[:R].astype(np.int32).reshape(R, 1)
+    s = np.zeros(R, np.int32)
+    e = np.full(R, 3, np.int32)
+    marks = kv.new_marks(nb, dev())
+    dup = bt.copy()
+    dup[R - 1, 0] = dup[0, 0]
+    assert oracle.validate_targets(shape, nb, dup, s, e) == \
+        kv.LUMEN_ERR_DUP_BLOCK
+    assert gpu_validate(shape, nb, dup, s, e, marks) == kv.LUMEN_ERR_DUP_BLOCK
+    assert gpu_validate(shape, nb, bt, s, e, marks) == kv.LUMEN_OK
+
+
+def test_validate_workload_tables():
+    """Serving-size tables: every restore wave of the restore burst and the
+    in-place table of the 70B TP shard validate; the burst's requests all at
+    once do not, because later waves reuse the blocks earlier waves freed."""
+    w = W.c3_restore()
+    for wave in W.restore_waves(w):
+        s, e = w.starts[0][wave], w.ends[0][wave]
+        bt = w.dst_block_tables[wave]
+        assert gpu_validate(w.shape, w.dst_num_blocks, bt, s, e) == kv.LUMEN_OK
+    s, e = w.starts[0], w.ends[0]
+    want = oracle.validate_targets(w.shape, w.dst_num_blocks,
+                                   w.dst_block_tables, s, e)
+    assert want == kv.LUMEN_ERR_DUP_BLOCK
+    assert gpu_validate(w.shape, w.dst_num_blocks, w.dst_block_tables, s,
+                        e) == want
+    w = W.c4_llama70b_tp8()
+    assert gpu_validate(w.shape, w.num_blocks, w.dst_block_tables,
+                        w.starts[0], w.ends[0]) == kv.LUMEN_OK

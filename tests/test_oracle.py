@@ -53,6 +53,23 @@ MUTANTS = [
      "static int worse(int a, int b) { return a ? a : b; }"),
     ("head dim reversed", "* H + h) * D + d;\n}\n\nstatic int worse",
      "* H + h) * D + (D - 1 - d);\n}\n\nstatic int worse"),
+    ("validate takes one page too many",
+     "int64_t last = (end[r] - 1) / sh->block_size;",
+     "int64_t last = end[r] / sh->block_size;"),
+    ("validate starts at page 0", "int64_t first = start[r] / sh->block_size;",
+     "int64_t first = 0;"),
+    ("validate needs three owners", "if (times[b] > 1)", "if (times[b] > 2)"),
+    ("validate ignores bad ranges",
+     "status = worse(status, ORACLE_ERR_RANGE);\n            continue;\n"
+     "        }\n        if (end[r] == start[r])",
+     "continue;\n        }\n        if (end[r] == start[r])"),
+    ("validate pool bound off by one",
+     "if (b < 0 || b >= sh->num_blocks) {\n                status = worse("
+     "status, ORACLE_ERR_BLOCK_ID);\n                continue;\n            }"
+     "\n            times[b]",
+     "if (b < 0 || b > sh->num_blocks) {\n                status = worse("
+     "status, ORACLE_ERR_BLOCK_ID);\n                continue;\n            }"
+     "\n            times[b]"),
 ]
 
 
@@ -67,6 +84,7 @@ try:
     P.pin_invariants(lib)
     P.pin_torch_indexing(lib)
     P.pin_error_codes(lib)
+    P.pin_validate_targets(lib, exhaustive=False)
 except AssertionError as exc:
     print("PINS_FAIL", repr(exc)[:200])
     sys.exit(0)

@@ -8,10 +8,15 @@
 // and never looks at values).  The copy is split into units of
 // (token row, layer): one unit is the K and V of one token in one layer,
 // 2*H*D*E bytes, contiguous on the checkpoint side.  Units are numbered in
-// checkpoint order, u = packed_row * L + layer, and a persistent grid of
-// wavefronts splits [0, total_units) into equal contiguous spans, so every
-// wavefront moves the same number of bytes whatever the mix of request
-// lengths.  Inside its span a wavefront walks token rows in order: the
+// checkpoint order, u = packed_row * L + layer, and the grid's wavefronts
+// split [0, total_units) into equal contiguous spans, so every wavefront
+// moves the same number of bytes whatever the mix of request lengths.  The
+// grid is oversubscribed (hundreds of wavefronts per CU, about one unit each
+// on a decode step): wavefronts that share a workload still run at very
+// different speeds on this chip, and short-lived ones let the hardware
+// dispatcher hand the remaining work to whichever CU frees a slot first,
+// where a grid of resident long-lived wavefronts ends on its slowest one.
+// Inside its span a wavefront walks token rows in order: the
 // request, its block-table entry and the checkpoint row of each token are
 // wave-uniform and live in scalar registers; the 64 lanes then move the
 // token's units as 16-byte vectors.  On the checkpoint side those vectors
@@ -46,15 +51,19 @@ namespace {
 #ifndef LUMEN_KV_CKPT_UNPACK_NT
 #define LUMEN_KV_CKPT_UNPACK_NT 3
 #endif
+// Wavefronts per CU in the copy grid (the environment variable of the same
+// name overrides it at run time).  Measured on the decode workload: 32 per
+// CU, about one resident round, gives 5.25 TB/s on the gather; 384 gives
+// 5.7-5.8 TB/s; far beyond one unit per wave, idle waves cost dispatch time.
 #ifndef LUMEN_KV_CKPT_WAVES_PER_CU
-#define LUMEN_KV_CKPT_WAVES_PER_CU 32
+#define LUMEN_KV_CKPT_WAVES_PER_CU 384
 #endif
-// Waves per SIMD the register allocation of the copy kernels must allow
-// (0: compiler's choice).
 // Double-buffer the batches of a row segment (1) or not (0).
 #ifndef LUMEN_KV_CKPT_PIPELINE
 #define LUMEN_KV_CKPT_PIPELINE 1
 #endif
+// Waves per SIMD the register allocation of the copy kernels must allow
+// (0: compiler's choice).
 #ifndef LUMEN_KV_CKPT_WAVES_PER_EU
 #define LUMEN_KV_CKPT_WAVES_PER_EU 0
 #endif
@@ -325,7 +334,7 @@ __device__ __forceinline__ int row_status(bool past, int32_t entry,
   return LUMEN_OK;
 }
 
-// One persistent kernel for both directions.  kPack: cache -> checkpoint;
+// One kernel for both directions.  kPack: cache -> checkpoint;
 // otherwise checkpoint -> cache.
 template <bool kPack, bool kHeadMajor>
 __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_kernel(
@@ -558,7 +567,7 @@ int waves_per_cu() {
   static int w = [] {
     const char *e = getenv("LUMEN_KV_CKPT_WAVES_PER_CU");
     int v = e ? atoi(e) : kDefaultWavesPerCU;
-    return v > 0 && v <= 64 ? v : kDefaultWavesPerCU;
+    return v > 0 && v <= 4096 ? v : kDefaultWavesPerCU;
   }();
   return w;
 }
@@ -652,8 +661,10 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   g.div_bs = make_fastdiv(uint32_t(bs));
 
   WsView v = ws_view(ws, num_reqs);
-  // Persistent grid: enough waves to keep every CU's memory pipeline full,
-  // and never more waves than the checkpoint could hold units.
+  // Oversubscribed grid (LUMEN_KV_CKPT_WAVES_PER_CU per CU), never more
+  // waves than the checkpoint buffer could hold units: a wave whose span is
+  // empty still costs a dispatch, so a checkpoint buffer sized to the rows
+  // of the plan keeps small launches from paying for idle waves.
   int64_t waves = int64_t(dev->cus) * waves_per_cu();
   const int64_t max_units = ckpt_rows * int64_t(lay->num_layers);
   if (max_units < waves) waves = max_units > 0 ? max_units : 1;

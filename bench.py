@@ -16,12 +16,15 @@ before timing; the device error word is checked after the timed loop.
 
 Further legs (reported beside the headline, not part of its value):
   * qwen-gqa-hnd    the same decode loop on the head-major Qwen-style cache
+  * qwen-gqa-nhd-twin  the same requests and tables over a token-major cache
+                    (what the head-major transpose costs)
   * restore-burst   64 interrupted requests restored into a 60%-occupied
                     pool; ms per restored request
   * tp8-shard       full pack and in-place unpack of one TP=8 rank of a
                     Llama-3-70B-shaped cache, the packed rows streamed to a
                     pinned host ring on a side stream during the pack
-  * cpu_baseline    the CPU oracle on a bounded sample of the decode workload
+  * cpu_baseline    the CPU oracle on a bounded sample of the decode workload,
+                    on one thread and split over the host's threads
 
 Bytes are algorithmic: 2 x tokens x token_row_bytes (read + write),
 decimal GB; peak is MI355X's 8 TB/s.
@@ -29,6 +32,7 @@ decimal GB; peak is MI355X's 8 TB/s.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import sys
@@ -173,6 +177,10 @@ def incremental_leg(torch, kv, w, steps, warmup, seed):
         unpack_us_mean=float(unpack_ms.mean() * 1e3),
         pack_us_median=float(np.median(pack_ms) * 1e3),
         unpack_us_median=float(np.median(unpack_ms) * 1e3),
+        pack_us_p10_p90=[float(np.percentile(pack_ms, q) * 1e3)
+                         for q in (10, 90)],
+        unpack_us_p10_p90=[float(np.percentile(unpack_ms, q) * 1e3)
+                           for q in (10, 90)],
         pack_bytes_mean=float(pack_b.mean()),
         unpack_bytes_mean=float(unpack_b.mean()),
         tokens_per_step_mean=float(rows.mean()),
@@ -371,11 +379,23 @@ def calibrate_copy(torch, mib):
 
 # ------------------------------------------------------------ CPU baseline
 
+def cpu_threads():
+    """Host threads the oracle may use: the process's CPU affinity, capped
+    by OMP_NUM_THREADS when the environment sets it (the GPU machine's share)."""
+    n = len(os.sched_getaffinity(0))
+    cap = os.environ.get("OMP_NUM_THREADS")
+    return max(1, min(n, int(cap))) if cap and cap.isdigit() else n
+
+
 def cpu_baseline(W, seconds):
-    """The CPU oracle (plain loops, one thread) on a bounded sample of the
-    same decode workload: whole steps packed from a host pool holding only
-    the blocks those steps read, until the time budget is spent."""
+    """The CPU oracle (plain loops) on a bounded sample of the same decode
+    workload: whole steps packed from a host pool holding only the blocks
+    those steps read, until the time budget is spent.  First on one thread,
+    then with the requests of each step split over the host's threads (the
+    oracle's C code runs outside the interpreter lock); the threaded figure
+    is the baseline."""
     import oracle
+    from concurrent.futures import ThreadPoolExecutor
     w = W.c2_llama8b()
     sh = w.shape
     bs = sh.block_size
@@ -394,22 +414,45 @@ def cpu_baseline(W, seconds):
         tables.append((len(pages), bt))
     nb = max(n for n, _ in tables)
     pool = W.random_bits(np.random.default_rng(0), sh.pool_elems(nb))
-    done_b, done_t, n_steps = 0.0, 0.0, 0
-    for k, (n, bt) in enumerate(tables):
-        t0 = time.perf_counter()
-        st, _ = oracle.pack(sh, nb, pool, bt, w.starts[k], w.ends[k])
-        done_t += time.perf_counter() - t0
-        assert st == 0
-        done_b += 2.0 * w.step_tokens(k) * sh.token_row_bytes
-        n_steps += 1
-        if done_t > seconds:
-            break
-    return {"value": round(gb(done_b) / done_t, 4), "unit": "GB/s",
-            "cores": 1, "kind": "oracle",
-            "sample": f"pack of decode steps 0..{n_steps - 1} of the "
-                      f"Llama-3-8B-shaped workload ({gb(done_b):.2f} GB read+"
+    lib = oracle.load()
+
+    def run(threads, budget):
+        bounds = np.linspace(0, w.num_reqs, threads + 1).astype(int)
+        done_b, done_t, n_steps = 0.0, 0.0, 0
+        with ThreadPoolExecutor(threads) as ex:
+            for k, (n, bt) in enumerate(tables):
+                s, e = w.starts[k], w.ends[k]
+                lens = (e.astype(np.int64) - s)
+                first = np.concatenate([[0], np.cumsum(lens)])
+                ck = np.empty((int(first[-1]), sh.token_row_elems), np.uint16)
+
+                def part(i):
+                    r0, r1 = bounds[i], bounds[i + 1]
+                    return oracle.pack(sh, nb, pool, bt[r0:r1], s[r0:r1],
+                                       e[r0:r1], row_base=int(first[r0]),
+                                       ckpt=ck, lib=lib)[0]
+                t0 = time.perf_counter()
+                sts = list(ex.map(part, range(threads)))
+                done_t += time.perf_counter() - t0
+                assert all(x == 0 for x in sts)
+                done_b += 2.0 * w.step_tokens(k) * sh.token_row_bytes
+                n_steps += 1
+                if done_t > budget:
+                    break
+        return gb(done_b) / done_t, n_steps, done_b
+
+    one, n1, b1 = run(1, seconds / 2)
+    threads = cpu_threads()
+    many, n2, b2 = run(threads, seconds / 2)
+    return {"value": round(many, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"pack of decode steps 0..{n2 - 1} of the "
+                      f"Llama-3-8B-shaped workload ({gb(b2):.2f} GB read+"
                       "written) from a compact host pool of the blocks those "
-                      "steps read"}
+                      f"steps read, requests split over {threads} threads",
+            "single_thread_value": round(one, 4),
+            "single_thread_sample": f"decode steps 0..{n1 - 1} "
+                                    f"({gb(b1):.2f} GB)"}
 
 
 # -------------------------------------------------------------------- main
@@ -437,8 +480,13 @@ def measured_traffic(kernel):
 
 
 def rounded(d):
-    return {k: (round(v, 4) if isinstance(v, float) else v)
-            for k, v in d.items()}
+    def r(v):
+        if isinstance(v, float):
+            return round(v, 4)
+        if isinstance(v, list):
+            return [r(x) for x in v]
+        return v
+    return {k: r(v) for k, v in d.items()}
 
 
 def main():
@@ -498,8 +546,17 @@ def main():
     }
     if "qwen" in legs:
         say("[bench] decode leg (qwen-gqa-hnd)")
+        q = W.c5_qwen_hnd()
         out["workloads"]["qwen-gqa-hnd"] = rounded(incremental_leg(
-            torch, kv, W.c5_qwen_hnd(), 64, 8, seed=5))
+            torch, kv, q, 64, 8, seed=5))
+        # the same requests and tables over a token-major cache: the
+        # difference is what the head-major transpose costs
+        twin = dataclasses.replace(
+            q, name="qwen-gqa-nhd-twin",
+            shape=dataclasses.replace(q.shape, order="NHD"))
+        say("[bench] decode leg (qwen-gqa-nhd-twin)")
+        out["workloads"]["qwen-gqa-nhd-twin"] = rounded(incremental_leg(
+            torch, kv, twin, 64, 8, seed=5))
     if "restore" in legs:
         say("[bench] restore leg")
         res = restore_leg(torch, kv, W)

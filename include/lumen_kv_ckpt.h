@@ -20,6 +20,14 @@
  *           device->pinned-host and pinned-host->device copies of packed
  *           rows on a side stream, ordered after (before) the main stream's
  *           work (the pinned CPU buffer of Sec. 4.2)
+ *   pack_rows / unpack_rows
+ *           a row range of a plan through a window of the checkpoint
+ *   pack_to_host / unpack_from_host
+ *           chunked pipelines through a small device staging ring: pack
+ *           overlapped with the copy to host memory, and the copy from host
+ *           memory overlapped with the unpack
+ *   validate_targets
+ *           validate mode of a restore (duplicate target blocks)
  *
  * Layouts.  The cache is one allocation of elements of elem_bytes bytes
  * (2 for bf16/fp16, 1 for an 8-bit cache, 4 for fp32; always moved as raw
@@ -137,6 +145,77 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
                          int32_t num_reqs, void *d_workspace,
                          const void *d_ckpt, int64_t ckpt_rows,
                          lumen_stream_t stream);
+
+/* Part of a pack, through a window of the checkpoint.  Copies only the
+ * plan's packed rows [row_begin, row_end), clipped to the plan's total;
+ * packed row i is the i-th planned token in request order, so a sequence
+ * of calls over consecutive row ranges does the whole pack in pieces (the
+ * chunks of Sec. 4.2's pipelined copy to pinned host memory).  d_ckpt
+ * holds the checkpoint rows [ckpt_first_row, ckpt_first_row + ckpt_rows):
+ * the token of checkpoint row c goes to buffer row c - ckpt_first_row, and
+ * a row outside the window is a CAPACITY error.  With a packed-mode plan
+ * from row_base 0, checkpoint row = packed row, so the window of rows
+ * [row_begin, row_end) is exactly a buffer of row_end - row_begin rows.
+ * row_begin <= row_end, both >= 0, ckpt_first_row >= 0 (INVALID_ARG).
+ * lumen_kv_ckpt_pack is this call with rows [0, INT64_MAX) and window 0. */
+int lumen_kv_ckpt_pack_rows(const lumen_kv_layout *layout, const void *d_cache,
+                            const int32_t *d_block_tables, int32_t bt_cols,
+                            int32_t num_reqs, void *d_workspace,
+                            int64_t row_begin, int64_t row_end, void *d_ckpt,
+                            int64_t ckpt_first_row, int64_t ckpt_rows,
+                            lumen_stream_t stream);
+
+/* Part of an unpack, through a window of the checkpoint: the inverse of
+ * lumen_kv_ckpt_pack_rows, with the same row range and window rules. */
+int lumen_kv_ckpt_unpack_rows(const lumen_kv_layout *layout, void *d_cache,
+                              const int32_t *d_block_tables, int32_t bt_cols,
+                              int32_t num_reqs, void *d_workspace,
+                              int64_t row_begin, int64_t row_end,
+                              const void *d_ckpt, int64_t ckpt_first_row,
+                              int64_t ckpt_rows, lumen_stream_t stream);
+
+/* Checkpoint straight to host memory (Sec. 4.2, steps 3 and 4 on one GPU:
+ * the new tokens are copied out of GPU memory into a pinned CPU buffer by
+ * background work while serving continues).  The plan's rows are packed in
+ * chunks of slot_rows rows into a device staging ring of `slots` slots
+ * (d_staging: slots * slot_rows rows, 16-byte aligned) on pack_stream, and
+ * each chunk is copied to h_ckpt on copy_stream as soon as it is packed;
+ * a slot is reused only after its previous copy has finished, so at most
+ * `slots` chunks are in flight and the device needs no full-size
+ * checkpoint buffer.  h_ckpt (host, pinned for overlap) receives packed rows
+ * [0, total_rows) in order, row i at byte i * row_bytes.
+ * The plan must be packed-mode from row_base 0 and enqueued before (on
+ * pack_stream, or ordered before it); total_rows must equal its total (the
+ * caller knows it: the sum of its ranges).  Both streams must differ from
+ * the serving stream for the work to stay off it.  Returns after enqueuing;
+ * the copies are complete once copy_stream has drained.  1 <= slots <= 64,
+ * slot_rows >= 1 (INVALID_ARG).  Device errors go to the workspace word. */
+int lumen_kv_ckpt_pack_to_host(const lumen_kv_layout *layout,
+                               const void *d_cache,
+                               const int32_t *d_block_tables, int32_t bt_cols,
+                               int32_t num_reqs, void *d_workspace,
+                               int64_t total_rows, void *d_staging,
+                               int64_t slot_rows, int32_t slots, void *h_ckpt,
+                               lumen_stream_t pack_stream,
+                               lumen_stream_t copy_stream);
+
+/* Restore straight from host memory (Sec. 4.3, loading the checkpointed
+ * pages back into GPU memory): the inverse pipeline.  Chunks of slot_rows
+ * rows of h_ckpt (packed rows in order, as lumen_kv_ckpt_pack_to_host
+ * writes them) are copied into the staging ring on copy_stream, and each is
+ * unpacked on unpack_stream as soon as it has arrived; a slot is refilled
+ * only after its previous unpack.  Same plan, total_rows and slot rules as
+ * lumen_kv_ckpt_pack_to_host; the restore is complete once unpack_stream
+ * has drained. */
+int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
+                                   void *d_cache,
+                                   const int32_t *d_block_tables,
+                                   int32_t bt_cols, int32_t num_reqs,
+                                   void *d_workspace, int64_t total_rows,
+                                   const void *h_ckpt, void *d_staging,
+                                   int64_t slot_rows, int32_t slots,
+                                   lumen_stream_t copy_stream,
+                                   lumen_stream_t unpack_stream);
 
 /* Bytes of the mark buffer lumen_kv_ckpt_validate_targets needs for a pool
  * of num_blocks blocks: one bit per block, rounded up to 16 bytes.  Returns

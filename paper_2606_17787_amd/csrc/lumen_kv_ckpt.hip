@@ -31,6 +31,7 @@
 #include <stdlib.h>
 
 #include <mutex>
+#include <vector>
 
 #include "lumen_kv_ckpt.h"
 
@@ -148,7 +149,10 @@ struct Geom {
   int64_t block_bytes;  // stride of one block inside a slab: bs*H*D*E
   int64_t row_bytes;    // one checkpoint row: L*2*H*D*E
   int64_t num_blocks;
-  int64_t ckpt_rows;
+  int64_t ckpt_rows;    // rows the checkpoint buffer (window) holds
+  int64_t win_first;    // checkpoint row held by buffer row 0
+  int64_t row_lo;       // packed rows [row_lo, row_hi) of the plan are copied
+  int64_t row_hi;
   int32_t num_layers;
   int32_t block_size;
   int32_t slot_bytes;   // stride of one slot: H*D*E (NHD) or D*E (HND)
@@ -353,9 +357,11 @@ __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_
     return;
   }
   const int64_t L = g.num_layers;
-  const int64_t units = hdr->total_rows * L;
-  int64_t u = units * gw / nw;
-  const int64_t u_end = units * (gw + 1) / nw;
+  const int64_t total = hdr->total_rows;
+  const int64_t row_a = min(g.row_lo, total), row_b = min(g.row_hi, total);
+  const int64_t units = (row_b - row_a) * L;
+  int64_t u = row_a * L + units * gw / nw;
+  const int64_t u_end = row_a * L + units * (gw + 1) / nw;
   if (u >= u_end) return;
 
   // First token row of the span and the request that owns it: the last
@@ -378,7 +384,7 @@ __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_
   const int64_t p0 = prefix[r];
   int64_t row_end = prefix[r + 1];
   int64_t t = start[r] + (row - p0);
-  int64_t crow = first_row[r] + (row - p0);
+  int64_t crow = first_row[r] + (row - p0) - g.win_first;  // buffer row
   if (g.bt_cols == 0) {  // every page lies past an empty table
     record_error(err, LUMEN_ERR_RANGE);
     return;
@@ -416,7 +422,7 @@ __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_
       } while (prefix[r2 + 1] == row + 1);
       row_end2 = prefix[r2 + 1];
       t2 = start[r2];
-      crow2 = first_row[r2];
+      crow2 = first_row[r2] - g.win_first;
     }
     bool past2;
     const int32_t b2 = block_tables[entry_index(r2, t2, g, past2)];
@@ -554,12 +560,19 @@ __global__ __launch_bounds__(kBlockThreads) void validate_kernel(
 // ------------------------------------------------------------- host side
 
 constexpr int kMaxDevices = 64;
+constexpr int32_t kMaxSlots = 64;  // ring slots of a staging pipeline
 
 struct DeviceInfo {
   std::once_flag once;
   int cus = 0;
   hipEvent_t order_event = nullptr;
   std::mutex event_mu;
+  // Events of the staging pipelines, two per ring slot, created on first
+  // use and kept for the life of the process.  pipe_mu is held while a
+  // pipeline enqueues, so two calls never interleave records and waits on
+  // the same event.
+  std::mutex pipe_mu;
+  std::vector<hipEvent_t> pipe_events;
 };
 DeviceInfo g_dev[kMaxDevices];
 
@@ -618,14 +631,15 @@ int check_layout(const lumen_kv_layout *lay) {
 
 int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
                 void *dst, const int32_t *bt, int32_t bt_cols,
-                int32_t num_reqs, void *ws, int64_t ckpt_rows,
-                lumen_stream_t stream) {
+                int32_t num_reqs, void *ws, int64_t row_lo, int64_t row_hi,
+                int64_t win_first, int64_t ckpt_rows, lumen_stream_t stream) {
   int st = check_layout(lay);
   if (st != LUMEN_OK) return st;
   if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0) return LUMEN_ERR_INVALID_ARG;
+  if (row_lo < 0 || row_hi < row_lo || win_first < 0) return LUMEN_ERR_INVALID_ARG;
   if (!ws) return LUMEN_ERR_INVALID_ARG;
   if (!aligned16(ws)) return LUMEN_ERR_MISALIGNED;
-  if (num_reqs == 0) return LUMEN_OK;
+  if (num_reqs == 0 || row_hi == row_lo) return LUMEN_OK;
   // A buffer may be null only when it is empty; the device checks then keep
   // every access away from it.
   const void *cache = pack ? src : dst;
@@ -647,6 +661,9 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   g.row_bytes = int64_t(lay->num_layers) * 2 * H * d_bytes;
   g.num_blocks = lay->num_blocks;
   g.ckpt_rows = ckpt_rows;
+  g.win_first = win_first;
+  g.row_lo = row_lo;
+  g.row_hi = row_hi;
   g.num_layers = lay->num_layers;
   g.block_size = lay->block_size;
   const bool hnd = lay->cache_order == LUMEN_CACHE_HND;
@@ -666,7 +683,9 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   // empty still costs a dispatch, so a checkpoint buffer sized to the rows
   // of the plan keeps small launches from paying for idle waves.
   int64_t waves = int64_t(dev->cus) * waves_per_cu();
-  const int64_t max_units = ckpt_rows * int64_t(lay->num_layers);
+  const int64_t max_units =
+      (ckpt_rows < row_hi - row_lo ? ckpt_rows : row_hi - row_lo) *
+      int64_t(lay->num_layers);
   if (max_units < waves) waves = max_units > 0 ? max_units : 1;
   const unsigned blocks = unsigned((waves + kWavesPerBlock - 1) / kWavesPerBlock);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -692,6 +711,31 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
                          v.prefix, v.first_row, v.start, &v.hdr->err, g);
   }
   return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
+}
+
+// Grows the device's pipeline event pool to n events; pipe_mu held.
+int pipe_events(DeviceInfo *dev, size_t n) {
+  while (dev->pipe_events.size() < n) {
+    hipEvent_t ev = nullptr;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess)
+      return LUMEN_ERR_HIP;
+    dev->pipe_events.push_back(ev);
+  }
+  return LUMEN_OK;
+}
+
+// Host-side checks shared by the two staging pipelines.
+int check_pipeline(const lumen_kv_layout *lay, int32_t num_reqs,
+                   const void *ws, int64_t total_rows, const void *staging,
+                   int64_t slot_rows, int32_t slots, const void *host) {
+  int st = check_layout(lay);
+  if (st != LUMEN_OK) return st;
+  if (num_reqs < 0 || total_rows < 0 || !ws) return LUMEN_ERR_INVALID_ARG;
+  if (slots < 1 || slots > kMaxSlots || slot_rows < 1)
+    return LUMEN_ERR_INVALID_ARG;
+  if (total_rows > 0 && (!staging || !host)) return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(ws) || !aligned16(staging)) return LUMEN_ERR_MISALIGNED;
+  return LUMEN_OK;
 }
 
 }  // namespace
@@ -725,7 +769,8 @@ int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
                        int32_t num_reqs, void *d_workspace, void *d_ckpt,
                        int64_t ckpt_rows, lumen_stream_t stream) {
   return launch_copy(true, layout, d_cache, d_ckpt, d_block_tables, bt_cols,
-                     num_reqs, d_workspace, ckpt_rows, stream);
+                     num_reqs, d_workspace, 0, INT64_MAX, 0, ckpt_rows,
+                     stream);
 }
 
 int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
@@ -734,7 +779,30 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
                          const void *d_ckpt, int64_t ckpt_rows,
                          lumen_stream_t stream) {
   return launch_copy(false, layout, d_ckpt, d_cache, d_block_tables, bt_cols,
-                     num_reqs, d_workspace, ckpt_rows, stream);
+                     num_reqs, d_workspace, 0, INT64_MAX, 0, ckpt_rows,
+                     stream);
+}
+
+int lumen_kv_ckpt_pack_rows(const lumen_kv_layout *layout, const void *d_cache,
+                            const int32_t *d_block_tables, int32_t bt_cols,
+                            int32_t num_reqs, void *d_workspace,
+                            int64_t row_begin, int64_t row_end, void *d_ckpt,
+                            int64_t ckpt_first_row, int64_t ckpt_rows,
+                            lumen_stream_t stream) {
+  return launch_copy(true, layout, d_cache, d_ckpt, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, row_begin, row_end,
+                     ckpt_first_row, ckpt_rows, stream);
+}
+
+int lumen_kv_ckpt_unpack_rows(const lumen_kv_layout *layout, void *d_cache,
+                              const int32_t *d_block_tables, int32_t bt_cols,
+                              int32_t num_reqs, void *d_workspace,
+                              int64_t row_begin, int64_t row_end,
+                              const void *d_ckpt, int64_t ckpt_first_row,
+                              int64_t ckpt_rows, lumen_stream_t stream) {
+  return launch_copy(false, layout, d_ckpt, d_cache, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, row_begin, row_end,
+                     ckpt_first_row, ckpt_rows, stream);
 }
 
 size_t lumen_kv_ckpt_marks_bytes(int64_t num_blocks) {
@@ -777,6 +845,97 @@ int lumen_kv_ckpt_validate_targets(const lumen_kv_layout *layout,
                      &v.hdr->err, num_reqs, bt_cols, layout->block_size,
                      layout->num_blocks);
   return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
+}
+
+int lumen_kv_ckpt_pack_to_host(const lumen_kv_layout *layout,
+                               const void *d_cache,
+                               const int32_t *d_block_tables, int32_t bt_cols,
+                               int32_t num_reqs, void *d_workspace,
+                               int64_t total_rows, void *d_staging,
+                               int64_t slot_rows, int32_t slots, void *h_ckpt,
+                               lumen_stream_t pack_stream,
+                               lumen_stream_t copy_stream) {
+  int st = check_pipeline(layout, num_reqs, d_workspace, total_rows, d_staging,
+                          slot_rows, slots, h_ckpt);
+  if (st != LUMEN_OK || total_rows == 0 || num_reqs == 0) return st;
+  DeviceInfo *dev = nullptr;
+  st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  const int64_t row_bytes = int64_t(layout->num_layers) * 2 *
+                            layout->num_kv_heads * layout->head_dim *
+                            layout->elem_bytes;
+  hipStream_t ps = static_cast<hipStream_t>(pack_stream);
+  hipStream_t cs = static_cast<hipStream_t>(copy_stream);
+  std::lock_guard<std::mutex> lock(dev->pipe_mu);
+  st = pipe_events(dev, 2 * size_t(slots));
+  if (st != LUMEN_OK) return st;
+  hipEvent_t *packed = dev->pipe_events.data();
+  hipEvent_t *copied = packed + slots;
+  for (int64_t c = 0, lo = 0; lo < total_rows; ++c, lo += slot_rows) {
+    const int64_t hi = lo + slot_rows < total_rows ? lo + slot_rows : total_rows;
+    const int32_t j = int32_t(c % slots);
+    uint8_t *slot = static_cast<uint8_t *>(d_staging) + j * slot_rows * row_bytes;
+    // A slot is packed again only after its previous rows reached the host.
+    if (c >= slots && hipStreamWaitEvent(ps, copied[j], 0) != hipSuccess)
+      return LUMEN_ERR_HIP;
+    st = launch_copy(true, layout, d_cache, slot, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, lo, hi, lo, slot_rows, ps);
+    if (st != LUMEN_OK) return st;
+    if (hipEventRecord(packed[j], ps) != hipSuccess ||
+        hipStreamWaitEvent(cs, packed[j], 0) != hipSuccess ||
+        hipMemcpyAsync(static_cast<uint8_t *>(h_ckpt) + lo * row_bytes, slot,
+                       size_t((hi - lo) * row_bytes), hipMemcpyDeviceToHost,
+                       cs) != hipSuccess ||
+        hipEventRecord(copied[j], cs) != hipSuccess)
+      return LUMEN_ERR_HIP;
+  }
+  return LUMEN_OK;
+}
+
+int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
+                                   void *d_cache,
+                                   const int32_t *d_block_tables,
+                                   int32_t bt_cols, int32_t num_reqs,
+                                   void *d_workspace, int64_t total_rows,
+                                   const void *h_ckpt, void *d_staging,
+                                   int64_t slot_rows, int32_t slots,
+                                   lumen_stream_t copy_stream,
+                                   lumen_stream_t unpack_stream) {
+  int st = check_pipeline(layout, num_reqs, d_workspace, total_rows, d_staging,
+                          slot_rows, slots, h_ckpt);
+  if (st != LUMEN_OK || total_rows == 0 || num_reqs == 0) return st;
+  DeviceInfo *dev = nullptr;
+  st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  const int64_t row_bytes = int64_t(layout->num_layers) * 2 *
+                            layout->num_kv_heads * layout->head_dim *
+                            layout->elem_bytes;
+  hipStream_t cs = static_cast<hipStream_t>(copy_stream);
+  hipStream_t us = static_cast<hipStream_t>(unpack_stream);
+  std::lock_guard<std::mutex> lock(dev->pipe_mu);
+  st = pipe_events(dev, 2 * size_t(slots));
+  if (st != LUMEN_OK) return st;
+  hipEvent_t *staged = dev->pipe_events.data();
+  hipEvent_t *drained = staged + slots;
+  for (int64_t c = 0, lo = 0; lo < total_rows; ++c, lo += slot_rows) {
+    const int64_t hi = lo + slot_rows < total_rows ? lo + slot_rows : total_rows;
+    const int32_t j = int32_t(c % slots);
+    uint8_t *slot = static_cast<uint8_t *>(d_staging) + j * slot_rows * row_bytes;
+    // A slot is refilled only after the unpack of its previous rows.
+    if (c >= slots && hipStreamWaitEvent(cs, drained[j], 0) != hipSuccess)
+      return LUMEN_ERR_HIP;
+    if (hipMemcpyAsync(slot, static_cast<const uint8_t *>(h_ckpt) + lo * row_bytes,
+                       size_t((hi - lo) * row_bytes), hipMemcpyHostToDevice,
+                       cs) != hipSuccess ||
+        hipEventRecord(staged[j], cs) != hipSuccess ||
+        hipStreamWaitEvent(us, staged[j], 0) != hipSuccess)
+      return LUMEN_ERR_HIP;
+    st = launch_copy(false, layout, slot, d_cache, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, lo, hi, lo, slot_rows, us);
+    if (st != LUMEN_OK) return st;
+    if (hipEventRecord(drained[j], us) != hipSuccess) return LUMEN_ERR_HIP;
+  }
+  return LUMEN_OK;
 }
 
 int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream) {

@@ -83,6 +83,18 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_unpack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
         "lumen_kv_ckpt_status": (ctypes.c_int, [p, p]),
         "lumen_kv_ckpt_marks_bytes": (sz, [i64]),
+        "lumen_kv_ckpt_pack_rows": (ctypes.c_int,
+                                    [lay, p, p, i32, i32, p, i64, i64, p, i64,
+                                     i64, p]),
+        "lumen_kv_ckpt_unpack_rows": (ctypes.c_int,
+                                      [lay, p, p, i32, i32, p, i64, i64, p,
+                                       i64, i64, p]),
+        "lumen_kv_ckpt_pack_to_host": (ctypes.c_int,
+                                       [lay, p, p, i32, i32, p, i64, p, i64,
+                                        i32, p, p, p]),
+        "lumen_kv_ckpt_unpack_from_host": (ctypes.c_int,
+                                           [lay, p, p, i32, i32, p, i64, p, p,
+                                            i64, i32, p, p]),
         "lumen_kv_ckpt_validate_targets": (ctypes.c_int,
                                            [lay, p, i32, i32, p, p, sz, p]),
         "lumen_kv_ckpt_strerror": (ctypes.c_char_p, [ctypes.c_int]),
@@ -231,6 +243,123 @@ def lumen_kv_ckpt_unpack(shape, num_blocks: int, cache: torch.Tensor,
     """Scatter the planned checkpoint rows of `ckpt` into `cache`."""
     _copy("lumen_kv_ckpt_unpack", shape, num_blocks, cache, block_tables,
           workspace, ckpt, stream)
+
+
+def _rows_call(name: str, shape, num_blocks: int, cache: torch.Tensor,
+               block_tables: torch.Tensor, workspace: torch.Tensor,
+               row_begin: int, row_end: int, ckpt: torch.Tensor,
+               ckpt_first_row: int, stream):
+    R = block_tables.shape[0] if block_tables.dim() == 2 else -1
+    _check_tables(block_tables, R)
+    _check_cache(shape, num_blocks, cache, "cache")
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    if (ckpt.element_size() != _elem_bytes(shape)
+            or ckpt.numel() % _row_elems(shape)):
+        raise ValueError("checkpoint window must hold whole rows of "
+                         f"{_elem_bytes(shape)}-byte elements")
+    rows = ckpt.numel() // _row_elems(shape)
+    lay = layout(shape, num_blocks)
+    _check(getattr(load_library(), name)(
+        ctypes.byref(lay), _dev(cache, "cache"),
+        _dev(block_tables, "block_tables", torch.int32),
+        block_tables.shape[1], R, _dev(workspace, "workspace"),
+        int(row_begin), int(row_end), _dev(ckpt, "ckpt"),
+        int(ckpt_first_row), rows, _stream_handle(stream)), name)
+
+
+INT64_MAX = (1 << 63) - 1
+
+
+def lumen_kv_ckpt_pack_rows(shape, num_blocks: int, cache: torch.Tensor,
+                            block_tables: torch.Tensor,
+                            workspace: torch.Tensor, row_begin: int,
+                            row_end: int, ckpt: torch.Tensor,
+                            ckpt_first_row: int = 0,
+                            stream: Optional[torch.cuda.Stream] = None):
+    """Pack the plan's packed rows [row_begin, row_end) into `ckpt`, a window
+    holding checkpoint rows [ckpt_first_row, ckpt_first_row + rows)."""
+    _rows_call("lumen_kv_ckpt_pack_rows", shape, num_blocks, cache,
+               block_tables, workspace, row_begin, row_end, ckpt,
+               ckpt_first_row, stream)
+
+
+def lumen_kv_ckpt_unpack_rows(shape, num_blocks: int, cache: torch.Tensor,
+                              block_tables: torch.Tensor,
+                              workspace: torch.Tensor, row_begin: int,
+                              row_end: int, ckpt: torch.Tensor,
+                              ckpt_first_row: int = 0,
+                              stream: Optional[torch.cuda.Stream] = None):
+    """Unpack the plan's packed rows [row_begin, row_end) from the window."""
+    _rows_call("lumen_kv_ckpt_unpack_rows", shape, num_blocks, cache,
+               block_tables, workspace, row_begin, row_end, ckpt,
+               ckpt_first_row, stream)
+
+
+def _pipeline_args(shape, num_blocks, cache, block_tables, workspace,
+                   total_rows, staging, slots, host):
+    R = block_tables.shape[0] if block_tables.dim() == 2 else -1
+    _check_tables(block_tables, R)
+    _check_cache(shape, num_blocks, cache, "cache")
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    rb = _row_elems(shape) * _elem_bytes(shape)
+    if host.is_cuda or not host.is_contiguous():
+        raise ValueError("host checkpoint must be a contiguous host tensor")
+    if _nbytes(host) < int(total_rows) * rb:
+        raise ValueError("host checkpoint smaller than total_rows rows")
+    if slots < 1 or _nbytes(staging) % (slots * rb):
+        raise ValueError("staging must hold `slots` slots of whole rows")
+    slot_rows = _nbytes(staging) // (slots * rb)
+    if slot_rows < 1:
+        raise ValueError("staging holds no row per slot")
+    return R, slot_rows
+
+
+def lumen_kv_ckpt_pack_to_host(shape, num_blocks: int, cache: torch.Tensor,
+                               block_tables: torch.Tensor,
+                               workspace: torch.Tensor, total_rows: int,
+                               staging: torch.Tensor, slots: int,
+                               host: torch.Tensor,
+                               pack_stream: Optional[torch.cuda.Stream] = None,
+                               copy_stream: Optional[torch.cuda.Stream] = None):
+    """Pack the planned rows through a device staging ring of `slots` equal
+    slots (`staging` is split evenly) into host tensor `host` (pinned)."""
+    R, slot_rows = _pipeline_args(shape, num_blocks, cache, block_tables,
+                                  workspace, total_rows, staging, slots, host)
+    lay = layout(shape, num_blocks)
+    _check(load_library().lumen_kv_ckpt_pack_to_host(
+        ctypes.byref(lay), _dev(cache, "cache"),
+        _dev(block_tables, "block_tables", torch.int32),
+        block_tables.shape[1], R, _dev(workspace, "workspace"),
+        int(total_rows), _dev(staging, "staging"), slot_rows, int(slots),
+        ctypes.c_void_p(host.data_ptr()), _stream_handle(pack_stream),
+        _stream_handle(copy_stream)), "lumen_kv_ckpt_pack_to_host")
+
+
+def lumen_kv_ckpt_unpack_from_host(shape, num_blocks: int,
+                                   cache: torch.Tensor,
+                                   block_tables: torch.Tensor,
+                                   workspace: torch.Tensor, total_rows: int,
+                                   host: torch.Tensor, staging: torch.Tensor,
+                                   slots: int,
+                                   copy_stream: Optional[torch.cuda.Stream] = None,
+                                   unpack_stream: Optional[torch.cuda.Stream] = None):
+    """Restore the planned rows from host tensor `host` through the staging
+    ring into `cache`."""
+    R, slot_rows = _pipeline_args(shape, num_blocks, cache, block_tables,
+                                  workspace, total_rows, staging, slots, host)
+    lay = layout(shape, num_blocks)
+    _check(load_library().lumen_kv_ckpt_unpack_from_host(
+        ctypes.byref(lay), _dev(cache, "cache"),
+        _dev(block_tables, "block_tables", torch.int32),
+        block_tables.shape[1], R, _dev(workspace, "workspace"),
+        int(total_rows), ctypes.c_void_p(host.data_ptr()),
+        _dev(staging, "staging"), slot_rows, int(slots),
+        _stream_handle(copy_stream), _stream_handle(unpack_stream)),
+        "lumen_kv_ckpt_unpack_from_host")
 
 
 def lumen_kv_ckpt_marks_bytes(num_blocks: int) -> int:

@@ -165,3 +165,54 @@ def test_binding_checks_shapes_before_calling():
                               torch.zeros(2, 4, dtype=torch.int32),
                               torch.zeros(256, dtype=torch.uint8),
                               torch.zeros(512, dtype=torch.int16))
+
+
+def test_row_range_host_validation(lib):
+    for name in ("lumen_kv_ckpt_pack_rows", "lumen_kv_ckpt_unpack_rows"):
+        f = getattr(lib, name)
+
+        def call(lay=None, R=2, ws=FAKE, lo=0, hi=10, first=0, rows=10,
+                 ck=FAKE):
+            lay = _layout() if lay is None else lay
+            return f(ctypes.byref(lay), FAKE, FAKE, 4, R, ws, lo, hi, ck,
+                     first, rows, None)
+
+        assert call(lo=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(lo=5, hi=4) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(first=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(rows=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(ws=None) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(lay=_layout(elem_bytes=3)) == kv.LUMEN_ERR_UNSUPPORTED
+        assert call(ck=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+        # an empty row range or no requests enqueues nothing
+        assert call(lo=7, hi=7) == kv.LUMEN_OK
+        assert call(R=0) == kv.LUMEN_OK
+
+
+def test_pipeline_host_validation(lib):
+    for name in ("lumen_kv_ckpt_pack_to_host",
+                 "lumen_kv_ckpt_unpack_from_host"):
+        f = getattr(lib, name)
+        pack = name.endswith("to_host")
+
+        def call(R=2, ws=FAKE, total=100, staging=FAKE, slot_rows=8,
+                 slots=2, host=FAKE):
+            lay = _layout()
+            if pack:
+                return f(ctypes.byref(lay), FAKE, FAKE, 4, R, ws, total,
+                         staging, slot_rows, slots, host, None, None)
+            return f(ctypes.byref(lay), FAKE, FAKE, 4, R, ws, total, host,
+                     staging, slot_rows, slots, None, None)
+
+        assert call(slots=0) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(slots=65) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(slot_rows=0) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(total=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(ws=None) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(staging=None) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(host=None) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(staging=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+        assert call(ws=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+        # nothing to move: no HIP call at all
+        assert call(total=0, staging=None, host=None) == kv.LUMEN_OK
+        assert call(R=0) == kv.LUMEN_OK

@@ -1,0 +1,229 @@
+"""Row ranges, checkpoint windows and the host staging pipelines against the
+CPU oracle, element by element.
+
+A chunk of packed rows [lo, hi) of a plan is the plan's ranges clipped to
+those rows; packed from row_base 0 it fills rows [0, hi - lo), which is the
+window [lo, hi) of the checkpoint.  So every chunked call has an exact
+oracle counterpart, error codes included."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_17787_amd.kvckpt as kv
+from paper_2606_17787_amd import workloads as W
+from paper_2606_17787_amd.workloads import CacheShape, HND, NHD
+
+from gpu_util import SENTINEL, d2h_words, dev, h2d
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [CacheShape(2, 2, 64, 16, NHD), CacheShape(3, 2, 128, 32, HND),
+          CacheShape(1, 3, 40, 5, HND), CacheShape(2, 1, 16, 3, NHD, 1),
+          CacheShape(2, 2, 8, 4, NHD, 4)]
+WORD = {1: np.uint8, 2: np.uint16, 4: np.uint32}
+
+
+def clip_ranges(s, e, lo, hi):
+    """Per-request sub-ranges whose packed rows fall in [lo, hi)."""
+    n = np.maximum(e.astype(np.int64) - s, 0)
+    first = np.concatenate([[0], np.cumsum(n)[:-1]])
+    a = np.clip(lo - first, 0, n)
+    b = np.clip(hi - first, 0, n)
+    return (s + a).astype(np.int32), (s + b).astype(np.int32)
+
+
+def case(shape, seed, R=13, max_tok=90):
+    rng = np.random.default_rng(seed)
+    bs = shape.block_size
+    cols = -(-max_tok // bs) + 1
+    nb = R * cols + 5
+    bt = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    bt2 = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    s = rng.integers(0, max_tok, R).astype(np.int32)
+    e = np.minimum(s + rng.integers(0, 40, R), max_tok).astype(np.int32)
+    empty = rng.random(R) < 0.2
+    e[empty] = s[empty]
+    src = W.random_words(rng, shape.pool_elems(nb), shape.elem_bytes)
+    dst = W.random_words(rng, shape.pool_elems(nb), shape.elem_bytes)
+    return nb, bt, bt2, s, e, src, dst
+
+
+def planned(s, e):
+    """Plan on the current stream (the range tensors are freed after the
+    call, which is safe only for work on the stream they were made on)."""
+    ws = kv.new_workspace(len(s), dev())
+    kv.lumen_kv_ckpt_plan(h2d(s), h2d(e), ws)
+    return ws
+
+
+def window(shape, rows):
+    w = np.full(max(rows, 0) * shape.token_row_elems, SENTINEL,
+                WORD[shape.elem_bytes])
+    return h2d(w)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"bs{s.block_size}{s.order}e{s.elem_bytes}")
+def test_pack_rows_chunks(shape):
+    nb, bt, _, s, e, src, _ = case(shape, zlib.crc32(repr(shape).encode()))
+    total = int((e - s).sum())
+    d_src, d_bt = h2d(src), h2d(bt)
+    ws = planned(s, e)
+    for C in (1, 7, 64, total + 5):
+        for lo in range(0, total + 1, C):
+            hi = lo + C
+            for spare in (0, 2):
+                win = window(shape, C + spare)
+                kv.lumen_kv_ckpt_pack_rows(shape, nb, d_src, d_bt, ws, lo, hi,
+                                           win, ckpt_first_row=lo)
+                st = kv.lumen_kv_ckpt_status(ws)
+                cs, ce = clip_ranges(s, e, lo, hi)
+                want = np.full((C + spare, shape.token_row_elems), SENTINEL,
+                               WORD[shape.elem_bytes])
+                st_o, want = oracle.pack(shape, nb, src, bt, cs, ce,
+                                         ckpt=want)
+                assert st == st_o == 0, (C, lo, st, st_o)
+                got = d2h_words(win, shape.elem_bytes).reshape(want.shape)
+                assert np.array_equal(got, want), (C, lo, spare)
+
+
+def test_window_too_small_reports_capacity():
+    shape = SHAPES[0]
+    nb, bt, _, s, e, src, _ = case(shape, 5)
+    total = int((e - s).sum())
+    assert total > 12
+    ws = planned(s, e)
+    lo, hi = 3, 12
+    win = window(shape, hi - lo - 1)
+    kv.lumen_kv_ckpt_pack_rows(shape, nb, h2d(src), h2d(bt), ws, lo, hi, win,
+                               ckpt_first_row=lo)
+    cs, ce = clip_ranges(s, e, lo, hi)
+    st_o, _ = oracle.pack(shape, nb, src, bt, cs, ce,
+                          ckpt_rows=hi - lo - 1,
+                          ckpt=np.zeros((hi - lo + 4, shape.token_row_elems),
+                                        np.uint16))
+    assert st_o == oracle.ERR_CAPACITY
+    assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_ERR_CAPACITY
+    # a window that starts past the chunk's rows misses every row
+    win = window(shape, 20)
+    ws = planned(s, e)
+    kv.lumen_kv_ckpt_pack_rows(shape, nb, h2d(src), h2d(bt), ws, lo, hi, win,
+                               ckpt_first_row=lo + 1)
+    assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_ERR_CAPACITY
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"bs{s.block_size}{s.order}e{s.elem_bytes}")
+def test_unpack_rows_chunks(shape):
+    nb, _, bt2, s, e, _, dst = case(shape, zlib.crc32(repr(shape).encode()) + 1)
+    total = int((e - s).sum())
+    rng = np.random.default_rng(3)
+    ck = W.random_words(rng, total * shape.token_row_elems, shape.elem_bytes)
+    want = dst.copy()
+    assert oracle.unpack(shape, nb, want, bt2, s, e,
+                         ck.reshape(total, -1)) == 0
+    for C in (1, 9, total + 1):
+        d_dst = h2d(dst)
+        ws = planned(s, e)
+        re = shape.token_row_elems
+        for lo in range(0, total, C):
+            hi = min(lo + C, total)
+            win = h2d(ck[lo * re:hi * re])
+            kv.lumen_kv_ckpt_unpack_rows(shape, nb, d_dst, h2d(bt2), ws, lo,
+                                         lo + C, win, ckpt_first_row=lo)
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+        assert np.array_equal(d2h_words(d_dst, shape.elem_bytes), want), C
+
+
+def pinned(a: np.ndarray) -> torch.Tensor:
+    t = torch.empty(a.nbytes, dtype=torch.uint8, pin_memory=True)
+    t.numpy()[:] = a.view(np.uint8).reshape(-1)
+    return t
+
+
+@pytest.mark.parametrize("shape", SHAPES[:3], ids=lambda s: f"bs{s.block_size}{s.order}")
+def test_pack_to_host_and_back(shape):
+    nb, bt, bt2, s, e, src, dst = case(shape, zlib.crc32(repr(shape).encode()) + 2,
+                                       R=29, max_tok=150)
+    total = int((e - s).sum())
+    rb = shape.token_row_bytes
+    st_o, want = oracle.pack(shape, nb, src, bt, s, e)
+    assert st_o == 0
+    want_dst = dst.copy()
+    assert oracle.unpack(shape, nb, want_dst, bt2, s, e, want) == 0
+    # every device tensor the side streams read stays referenced until they
+    # have drained (the caching allocator knows only the current stream)
+    d_src, d_bt, d_bt2 = h2d(src), h2d(bt), h2d(bt2)
+    d_s, d_e = h2d(s), h2d(e)
+    torch.cuda.synchronize()
+    pack_s, copy_s = torch.cuda.Stream(), torch.cuda.Stream()
+    for slots, slot_rows in ((1, 5), (2, 1), (2, 17), (3, 40), (2, total + 3)):
+        staging = torch.empty(slots * slot_rows * rb, dtype=torch.uint8,
+                              device=dev())
+        host = torch.zeros(total * rb + 64, dtype=torch.uint8,
+                           pin_memory=True)
+        ws = kv.new_workspace(len(s), dev())
+        torch.cuda.synchronize()
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws, stream=pack_s)
+        kv.lumen_kv_ckpt_pack_to_host(shape, nb, d_src, d_bt, ws, total,
+                                      staging, slots, host,
+                                      pack_stream=pack_s, copy_stream=copy_s)
+        copy_s.synchronize()
+        assert kv.lumen_kv_ckpt_status(ws, stream=pack_s) == 0
+        got = host.numpy()[:total * rb].view(want.dtype).reshape(want.shape)
+        assert np.array_equal(got, want), (slots, slot_rows)
+        assert not host.numpy()[total * rb:].any()
+        # and back from the host copy into another pool
+        d_dst = h2d(dst)
+        ws2 = kv.new_workspace(len(s), dev())
+        torch.cuda.synchronize()
+        unpack_s = torch.cuda.Stream()
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws2, stream=unpack_s)
+        kv.lumen_kv_ckpt_unpack_from_host(shape, nb, d_dst, d_bt2, ws2,
+                                          total, host, staging, slots,
+                                          copy_stream=copy_s,
+                                          unpack_stream=unpack_s)
+        unpack_s.synchronize()
+        assert kv.lumen_kv_ckpt_status(ws2, stream=unpack_s) == 0
+        assert np.array_equal(d2h_words(d_dst, shape.elem_bytes),
+                              want_dst), (slots, slot_rows)
+
+
+def test_restore_from_host_restore_burst_requests():
+    """Two whole requests of the restore-burst workload (4K-32K tokens of a
+    Llama-3-8B-shaped cache) restored from pinned host memory into their
+    fragmented blocks, against the oracle on a compact pool of those
+    blocks."""
+    w = W.c3_restore()
+    sh = w.shape
+    order = np.argsort(w.ctx)[:2]  # the two shortest, about 1 GB together
+    s, e = w.starts[0][order], w.ends[0][order]
+    bt = w.dst_block_tables[order]
+    total = int((e - s).sum())
+    rb = sh.token_row_bytes
+    rng = np.random.default_rng(31)
+    ck = W.random_bits(rng, total * sh.token_row_elems)
+    host = pinned(ck)
+    # compact pool: only the blocks the two requests own, relabelled
+    used = np.unique(bt[bt >= 0])
+    relabel = np.full(w.dst_num_blocks, -1, np.int32)
+    relabel[used] = np.arange(used.size, dtype=np.int32)
+    bt_c = np.where(bt >= 0, relabel[np.maximum(bt, 0)], -1).astype(np.int32)
+    nb = int(used.size)
+    pool = W.random_bits(rng, sh.pool_elems(nb))
+    want = pool.copy()
+    assert oracle.unpack(sh, nb, want, bt_c, s, e, ck.reshape(total, -1)) == 0
+    d_pool = h2d(pool)
+    staging = torch.empty(2 * 2048 * rb, dtype=torch.uint8, device=dev())
+    ws = kv.new_workspace(2, dev())
+    d_s, d_e, d_bt = h2d(s), h2d(e), h2d(bt_c)
+    torch.cuda.synchronize()
+    cs, us = torch.cuda.Stream(), torch.cuda.Stream()
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, stream=us)
+    kv.lumen_kv_ckpt_unpack_from_host(sh, nb, d_pool, d_bt, ws, total,
+                                      host, staging, 2, copy_stream=cs,
+                                      unpack_stream=us)
+    us.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws, stream=us) == 0
+    assert np.array_equal(d2h_words(d_pool, 2), want)

@@ -23,6 +23,9 @@ Further legs (reported beside the headline, not part of its value):
   * tp8-shard       full pack and in-place unpack of one TP=8 rank of a
                     Llama-3-70B-shaped cache, the packed rows streamed to a
                     pinned host ring on a side stream during the pack
+  * host staging    decode steps checkpointed straight to pinned host memory
+                    beside an HBM-bound decode stand-in (its slowdown), and
+                    every restore-burst request restored from host memory
   * cpu_baseline    the CPU oracle on a bounded sample of the decode workload,
                     on one thread and split over the host's threads
 
@@ -46,7 +49,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
-ALL_LEGS = ("decode", "qwen", "restore", "tp8", "cpu")
+ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "cpu")
 EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step
 
 
@@ -359,6 +362,227 @@ def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
                 pinned_ring=f"{ring} x {slot_bytes >> 30} GiB")
 
 
+def host_link_rates(torch, host, dev_buf, reps=3):
+    """Plain copies between a pinned host buffer and device memory (the
+    ceiling of the staging pipelines), GB/s each way."""
+    n = min(host.numel(), dev_buf.numel())
+    h, d = host[:n], dev_buf[:n]
+    res = {}
+    for name, (dst, src) in (("h2d", (d, h)), ("d2h", (h, d))):
+        dst.copy_(src, non_blocking=True)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            dst.copy_(src, non_blocking=True)
+        b.record()
+        b.synchronize()
+        res[name] = gb(n * reps) / (a.elapsed_time(b) / 1e3)
+    return res
+
+
+def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
+                host_slots=4):
+    """Host staging both ways.
+
+    Decode side: every step, a stand-in for the decode kernels reads the KV
+    the batch attends to (one HBM-bound pass over sum(ctx) token rows of the
+    source pool) on the serving stream, while that step's new tokens are
+    packed through a small device ring and copied to pinned host memory on
+    two other streams (lumen_kv_ckpt_pack_to_host).  Reported: the decode
+    stand-in's time alone and with checkpointing, and the sustained D2H.
+
+    Restore side: each of the 64 restore-burst requests is restored from a
+    pinned host copy of its checkpoint through the staging ring
+    (lumen_kv_ckpt_unpack_from_host): ms per request including the host
+    link, against the 26 GB/s GPU-to-CPU figure of the paper's simulator."""
+    dev = torch.device("cuda:0")
+    out = {}
+    # ---------------------------------------------------------- decode side
+    w = W.c2_llama8b()
+    sh = w.shape
+    S = w.num_steps
+    rb = sh.token_row_bytes
+    rows = np.array([w.step_tokens(k) for k in range(S)], np.int64)
+    g = torch.Generator(device=dev)
+    g.manual_seed(2)
+    src = torch.empty(sh.pool_elems(w.num_blocks), dtype=torch.bfloat16,
+                      device=dev)
+    src.normal_(generator=g)
+    bt = torch.from_numpy(w.block_tables).to(dev)
+    starts = [torch.from_numpy(a).to(dev) for a in w.starts]
+    ends = [torch.from_numpy(a).to(dev) for a in w.ends]
+    attend = int(w.starts[0].astype(np.int64).sum()) * sh.token_row_elems
+    attend = min(attend, src.numel())
+    kv_view = src[:attend]
+    staging = torch.empty(ring_slots * slot_rows * rb, dtype=torch.uint8,
+                          device=dev)
+    hosts = [torch.empty(int(rows.max()) * rb, dtype=torch.uint8,
+                         pin_memory=True) for _ in range(host_slots)]
+    wss = [kv.new_workspace(w.num_reqs, dev) for _ in range(host_slots)]
+    pack_s, copy_s = torch.cuda.Stream(), torch.cuda.Stream()
+    sink = torch.empty((), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    link = host_link_rates(torch, hosts[0], staging)
+
+    def decode_loop(ckpt):
+        evs = [(torch.cuda.Event(enable_timing=True),
+                torch.cuda.Event(enable_timing=True))
+               for _ in range(decode_steps)]
+        done = [None] * host_slots
+        lat = []  # (issue, host copy complete) per checkpointed step
+        c0, c1 = (torch.cuda.Event(enable_timing=True),
+                  torch.cuda.Event(enable_timing=True))
+        t0 = time.perf_counter()
+        for i in range(decode_steps):
+            evs[i][0].record()
+            torch.sum(kv_view, dim=0, dtype=torch.float32, out=sink)
+            evs[i][1].record()
+            if ckpt:
+                k, j = i % S, i % host_slots
+                if done[j] is not None:
+                    done[j].synchronize()  # the host drains slot j
+                if i == 0:
+                    c0.record(copy_s)
+                issued = torch.cuda.Event(enable_timing=True)
+                issued.record(pack_s)
+                kv.lumen_kv_ckpt_plan(starts[k], ends[k], wss[j],
+                                      stream=pack_s)
+                kv.lumen_kv_ckpt_pack_to_host(
+                    sh, w.num_blocks, src, bt, wss[j], int(rows[k]), staging,
+                    ring_slots, hosts[j], pack_stream=pack_s,
+                    copy_stream=copy_s)
+                ev = torch.cuda.Event(enable_timing=True)
+                ev.record(copy_s)
+                done[j] = ev
+                lat.append((issued, ev, int(rows[k])))
+        t_issue = time.perf_counter() - t0
+        if ckpt:
+            c1.record(copy_s)
+        torch.cuda.synchronize()
+        t_all = time.perf_counter() - t0
+        ms = np.array([a.elapsed_time(b) for a, b in evs])
+        res = {"decode_ms_mean": float(ms.mean()),
+               "decode_ms_median": float(np.median(ms)),
+               "wall_ms": t_all * 1e3, "issue_ms": t_issue * 1e3}
+        if ckpt:
+            for ws in wss:
+                assert kv.lumen_kv_ckpt_status(ws, stream=pack_s) == 0
+            res["ckpt_span_ms"] = c0.elapsed_time(c1)
+            res["ckpt_bytes"] = float(sum(rows[i % S] for i in
+                                          range(decode_steps)) * rb)
+            res["ckpt_latency_ms"] = np.array([a.elapsed_time(b)
+                                               for a, b, _ in lat])
+            res["ckpt_step_bytes"] = np.array([n * rb for _, _, n in lat],
+                                              np.float64)
+        return res
+
+    decode_loop(False)  # warm-up
+    alone = decode_loop(False)
+    withc = decode_loop(True)
+    # the last step's host copy against the device rows of that step
+    k = (decode_steps - 1) % S
+    j = (decode_steps - 1) % host_slots
+    ws = kv.new_workspace(w.num_reqs, dev)
+    kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws)
+    back = torch.empty(int(rows[k]) * rb, dtype=torch.uint8, device=dev)
+    kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws,
+                          back.view(torch.bfloat16))
+    ok = bool(torch.equal(back.cpu(), hosts[j][:back.numel()]))
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    decode_GBps = gb(kv_view.numel() * 2) / (alone["decode_ms_mean"] / 1e3)
+    out["decode_with_checkpoint"] = {
+        "workload": w.name, "decode_steps": decode_steps,
+        "decode_standin": "one HBM-bound pass over the KV of the batch "
+                          f"({gb(kv_view.numel() * 2):.1f} GB) per step",
+        "decode_standin_GBps": decode_GBps,
+        "decode_ms_alone": alone["decode_ms_mean"],
+        "decode_ms_with_checkpoint": withc["decode_ms_mean"],
+        "decode_slowdown": withc["decode_ms_mean"] / alone["decode_ms_mean"],
+        "wall_ms_alone": alone["wall_ms"],
+        "wall_ms_with_checkpoint": withc["wall_ms"],
+        "checkpoint_GB": gb(withc["ckpt_bytes"]),
+        "checkpoint_latency_ms_mean": float(withc["ckpt_latency_ms"].mean()),
+        "checkpoint_latency_ms_max": float(withc["ckpt_latency_ms"].max()),
+        "checkpoint_step_GBps": gb(withc["ckpt_step_bytes"].sum())
+        / (withc["ckpt_latency_ms"].sum() / 1e3),
+        "d2h_link_GBps": link["d2h"],
+        "staging_ring": f"{ring_slots} x {slot_rows} rows "
+                        f"({ring_slots * slot_rows * rb / 2**20:.0f} MiB)",
+        "host_copy_ok": ok}
+    del src, kv_view, staging, hosts, back
+    torch.cuda.empty_cache()
+    # --------------------------------------------------------- restore side
+    w = W.c3_restore()
+    sh = w.shape
+    rb = sh.token_row_bytes
+    ctx = w.ends[0].astype(np.int64)
+    waves = W.restore_waves(w)
+    pool = torch.zeros(sh.pool_elems(w.dst_num_blocks), dtype=torch.bfloat16,
+                       device=dev)
+    big = int(ctx.max())
+    host = torch.empty(big * rb, dtype=torch.uint8, pin_memory=True)
+    fill = torch.empty(big * sh.token_row_elems, dtype=torch.bfloat16,
+                       device=dev)
+    fill.normal_(generator=g)
+    host.copy_(fill.view(torch.uint8))
+    del fill
+    staging = torch.empty(ring_slots * slot_rows * rb, dtype=torch.uint8,
+                          device=dev)
+    cs, us = torch.cuda.Stream(), torch.cuda.Stream()
+    ws = kv.new_workspace(1, dev)
+    torch.cuda.synchronize()
+    per_ms = []
+    for wv in waves:
+        bt = torch.from_numpy(w.dst_block_tables[wv]).to(dev)
+        s_w = torch.from_numpy(w.starts[0][wv]).to(dev)
+        e_w = torch.from_numpy(w.ends[0][wv]).to(dev)
+        torch.cuda.synchronize()
+        for i, r in enumerate(wv):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            bt_r = bt[i:i + 1]  # a view: nothing for the side streams to outlive
+            kv.lumen_kv_ckpt_plan(s_w[i:i + 1], e_w[i:i + 1], ws, stream=us)
+            a.record(us)
+            cs.wait_stream(us)
+            kv.lumen_kv_ckpt_unpack_from_host(
+                sh, w.dst_num_blocks, pool, bt_r, ws, int(ctx[r]), host,
+                staging, ring_slots, copy_stream=cs, unpack_stream=us)
+            b.record(us)
+            b.synchronize()
+            per_ms.append(a.elapsed_time(b))
+            assert kv.lumen_kv_ckpt_status(ws, stream=us) == 0
+    # the last request, packed back from the pool, against the host bytes
+    r = int(waves[-1][-1])
+    ws2 = kv.new_workspace(1, dev)
+    kv.lumen_kv_ckpt_plan(torch.from_numpy(w.starts[0][[r]]).to(dev),
+                          torch.from_numpy(w.ends[0][[r]]).to(dev), ws2)
+    n = min(int(ctx[r]), 512)
+    back = torch.empty(int(ctx[r]) * rb, dtype=torch.uint8, device=dev)
+    kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, pool,
+                          torch.from_numpy(w.dst_block_tables[[r]]).to(dev),
+                          ws2, back.view(torch.bfloat16))
+    ok = bool(torch.equal(back[:n * rb].cpu(), host[:n * rb]))
+    assert kv.lumen_kv_ckpt_status(ws2) == 0
+    per_ms = np.array(per_ms)
+    req_b = ctx * rb
+    link = host_link_rates(torch, host, staging)
+    out["restore_from_host"] = {
+        "workload": w.name, "requests": int(len(per_ms)),
+        "h2d_link_GBps": link["h2d"],
+        "restore_ms_per_request": float(per_ms.mean()),
+        "restore_ms_per_request_median": float(np.median(per_ms)),
+        "h2d_GBps": gb(float(req_b.sum())) / (per_ms.sum() / 1e3),
+        "model_ms_per_request_at_26GBps": float(gb(req_b.mean()) / 26 * 1e3),
+        "staging_ring": f"{ring_slots} x {slot_rows} rows "
+                        f"({ring_slots * slot_rows * rb / 2**20:.0f} MiB)",
+        "spot_check_ok": ok}
+    del pool, host, staging, back
+    torch.cuda.empty_cache()
+    return out
+
+
 def calibrate_copy(torch, mib):
     """A plain device-to-device copy of known size: read + write bytes are
     exactly 2 * mib MiB per launch, the scale for the FETCH_SIZE/WRITE_SIZE
@@ -566,6 +790,10 @@ def main():
         say("[bench] tp8-shard leg")
         out["workloads"]["llama3-70b-tp8-shard"] = rounded(
             tp8_leg(torch, kv, W))
+    if "stage" in legs:
+        say("[bench] host staging leg")
+        for k2, v2 in staging_leg(torch, kv, W).items():
+            out["workloads"][k2] = rounded(v2)
     if "cpu" in legs:
         say("[bench] cpu baseline")
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)

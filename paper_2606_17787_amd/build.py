@@ -2,9 +2,10 @@
 
     python -m paper_2606_17787_amd.build
 
-compiles csrc/lumen_kv_ckpt.hip with hipcc into
+compiles csrc/lumen_kv_ckpt.hip (device kernels and their host entry
+points) and csrc/lumen_page_tags.cpp (host-only page tags) with hipcc into
 paper_2606_17787_amd/liblumen_kv_ckpt.so (position-independent, C ABI from
-include/lumen_kv_ckpt.h).
+include/lumen_kv_ckpt.h and include/lumen_page_tags.h).
 """
 from __future__ import annotations
 
@@ -15,6 +16,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "lumen_kv_ckpt.hip")
+SRC_TAGS = os.path.join(PKG, "csrc", "lumen_page_tags.cpp")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblumen_kv_ckpt.so")
 ARCH = "gfx950"
@@ -29,7 +31,8 @@ HIPCC_FLAGS = [
 
 def build(out: str = LIB, extra_flags=(), verbose: bool = False) -> str:
     hipcc = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
-    cmd = [hipcc, *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, SRC, "-o", out]
+    cmd = [hipcc, *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, SRC, SRC_TAGS,
+           "-o", out]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -24,7 +24,21 @@ def test_exports_every_declared_entry_point(lib):
                           "lumen_kv_ckpt_plan_workspace_bytes",
                           "lumen_kv_ckpt_offload", "lumen_kv_ckpt_stage_in",
                           "lumen_kv_ckpt_marks_bytes",
-                          "lumen_kv_ckpt_validate_targets"}
+                          "lumen_kv_ckpt_validate_targets",
+                          "lumen_kv_ckpt_pack_rows",
+                          "lumen_kv_ckpt_unpack_rows",
+                          "lumen_kv_ckpt_pack_to_host",
+                          "lumen_kv_ckpt_unpack_from_host"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_exports_every_page_tag_entry_point(lib):
+    from paper_2606_17787_amd import tags
+    names = tags.exported_names()
+    assert set(names) >= {"lumen_page_tags", "lumen_tag_store_create",
+                          "lumen_tag_store_publish",
+                          "lumen_tag_store_longest_prefix"}
     for n in names:
         assert hasattr(lib, n), n
 

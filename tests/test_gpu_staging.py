@@ -227,3 +227,77 @@ def test_restore_from_host_restore_burst_requests():
     us.synchronize()
     assert kv.lumen_kv_ckpt_status(ws, stream=us) == 0
     assert np.array_equal(d2h_words(d_pool, 2), want)
+
+
+def test_page_tags_drive_the_restore_of_a_cut_stream():
+    """Three requests are checkpointed to host memory in one pipeline.  The
+    stream is then cut after `cut` rows, which is forced from the host: only
+    pages wholly inside the rows received so far are published.  Recovery
+    regenerates each request's tags from its token history and restores the
+    longest contiguous prefix from host memory.  The tokens after it are
+    left for recomputation, and the pool must equal the oracle's restore of
+    exactly those prefixes."""
+    from oracle import tags as O
+    from paper_2606_17787_amd import tags as T
+    shape = CacheShape(2, 2, 64, 16, NHD)
+    bs = shape.block_size
+    rng = np.random.default_rng(77)
+    ctx = np.array([70, 33, 91], np.int32)
+    R = ctx.size
+    cols = -(-int(ctx.max()) // bs)
+    nb = R * cols + 3
+    bt = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    bt2 = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    s = np.zeros(R, np.int32)
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    hist = [rng.integers(0, 1 << 17, n).astype(np.int32) for n in ctx]
+    total = int(ctx.sum())
+    first = np.concatenate([[0], np.cumsum(ctx)[:-1]]).astype(np.int64)
+    rb = shape.token_row_bytes
+    d_src, d_bt, d_bt2 = h2d(src), h2d(bt), h2d(bt2)
+    d_s, d_e = h2d(s), h2d(ctx)
+    host = torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True)
+    staging = torch.empty(2 * 8 * rb, dtype=torch.uint8, device=dev())
+    ws = kv.new_workspace(R, dev())
+    torch.cuda.synchronize()
+    ps, cs = torch.cuda.Stream(), torch.cuda.Stream()
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, stream=ps)
+    kv.lumen_kv_ckpt_pack_to_host(shape, nb, d_src, d_bt, ws, total, staging,
+                                  2, host, pack_stream=ps, copy_stream=cs)
+    cs.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws, stream=ps) == 0
+    ck = host.numpy().view(np.uint16).reshape(total, -1)
+    for cut in (0, 5, 16, 70, 71, 100, 150, total):
+        nat, ora = T.TagStore(bs), O.TagStore(bs)
+        for r in range(R):
+            got = int(np.clip(cut - first[r], 0, ctx[r]))
+            pages = got // bs
+            nat.publish_pages(r, hist[r], 0, pages)
+            for i, tg in enumerate(O.page_tags(hist[r].tolist(), bs, 0,
+                                               pages)):
+                ora.publish(r, i, tg)
+        want = dst.copy()
+        d_dst = h2d(dst)
+        for r in range(R):
+            e_star = nat.longest_prefix(r, hist[r])
+            assert e_star == ora.longest_prefix(r, hist[r].tolist())
+            assert e_star == (int(np.clip(cut - first[r], 0, ctx[r])) // bs) * bs
+            if e_star == 0:
+                continue
+            assert oracle.unpack(shape, nb, want, bt2[r:r + 1], [0],
+                                 [e_star], ck[first[r]:first[r] + e_star]) == 0
+            d_e1 = h2d(np.array([e_star], np.int32))
+            d_s1 = h2d(np.array([0], np.int32))
+            d_btr = d_bt2[r:r + 1]
+            ws1 = kv.new_workspace(1, dev())
+            torch.cuda.synchronize()
+            us = torch.cuda.Stream()
+            kv.lumen_kv_ckpt_plan(d_s1, d_e1, ws1, stream=us)
+            kv.lumen_kv_ckpt_unpack_from_host(
+                shape, nb, d_dst, d_btr, ws1, e_star,
+                host[int(first[r]) * rb:], staging, 2, copy_stream=cs,
+                unpack_stream=us)
+            us.synchronize()
+            assert kv.lumen_kv_ckpt_status(ws1, stream=us) == 0
+        assert np.array_equal(d2h_words(d_dst, 2), want), cut

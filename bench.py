@@ -26,6 +26,7 @@ Further legs (reported beside the headline, not part of its value):
   * host staging    decode steps checkpointed straight to pinned host memory
                     beside an HBM-bound decode stand-in (its slowdown), and
                     every restore-burst request restored from host memory
+  * page tags       host-side tag generation and longest-prefix lookups
   * cpu_baseline    the CPU oracle on a bounded sample of the decode workload,
                     on one thread and split over the host's threads
 
@@ -49,7 +50,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
-ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "cpu")
+ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "tags", "cpu")
 EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step
 
 
@@ -583,6 +584,41 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
     return out
 
 
+def tags_leg(W):
+    """Host side of recovery (no GPU): tags of every complete page of the
+    decode workload's contexts, and longest-prefix lookups for the 64
+    restore-burst requests against a store holding all their pages."""
+    from paper_2606_17787_amd import tags as T
+    rng = np.random.default_rng(11)
+    w = W.c2_llama8b()
+    bs = w.shape.block_size
+    hists = [rng.integers(0, 128256, int(n)).astype(np.int32)
+             for n in w.starts[0]]
+    pages = sum(len(h) // bs for h in hists)
+    t0 = time.perf_counter()
+    for h in hists:
+        T.lumen_page_tags(h, bs)
+    t_tags = time.perf_counter() - t0
+    out = {"tags_pages": pages, "tags_ms": t_tags * 1e3,
+           "tags_Mpages_per_s": pages / t_tags / 1e6}
+    w = W.c3_restore()
+    bs = w.shape.block_size
+    store = T.TagStore(bs)
+    hists = [rng.integers(0, 128256, int(n)).astype(np.int32)
+             for n in w.ends[0]]
+    for r, h in enumerate(hists):
+        store.publish_pages(r, h, 0, len(h) // bs)
+    t0 = time.perf_counter()
+    got = [store.longest_prefix(r, h) for r, h in enumerate(hists)]
+    t_look = time.perf_counter() - t0
+    store.close()
+    assert got == [(len(h) // bs) * bs for h in hists]
+    out.update(lookup_requests=len(hists),
+               lookup_pages=sum(len(h) // bs for h in hists),
+               lookup_ms_per_request=t_look * 1e3 / len(hists))
+    return out
+
+
 def calibrate_copy(torch, mib):
     """A plain device-to-device copy of known size: read + write bytes are
     exactly 2 * mib MiB per launch, the scale for the FETCH_SIZE/WRITE_SIZE
@@ -794,6 +830,9 @@ def main():
         say("[bench] host staging leg")
         for k2, v2 in staging_leg(torch, kv, W).items():
             out["workloads"][k2] = rounded(v2)
+    if "tags" in legs:
+        say("[bench] page tags (host)")
+        out["workloads"]["page-tags"] = rounded(tags_leg(W))
     if "cpu" in legs:
         say("[bench] cpu baseline")
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)

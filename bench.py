@@ -27,6 +27,7 @@ Further legs (reported beside the headline, not part of its value):
                     beside an HBM-bound decode stand-in (its slowdown), and
                     every restore-burst request restored from host memory
   * page tags       host-side tag generation and longest-prefix lookups
+  * scheduler       host-side Eq. 1 placement and recovery events
   * cpu_baseline    the CPU oracle on a bounded sample of the decode workload,
                     on one thread and split over the host's threads
 
@@ -50,7 +51,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
-ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "tags", "cpu")
+ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "tags", "sched",
+            "cpu")
 EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step
 
 
@@ -619,6 +621,49 @@ def tags_leg(W):
     return out
 
 
+def sched_leg():
+    """Host side of placement and recovery (no GPU): Eq. 1 placement of
+    100,000 requests (4,000 active at a time, reserved footprints of
+    2K-16K Llama-3-8B-shaped tokens) over 64 workers with 80 GB checkpoint
+    budgets, then a recovery event that fails one worker and one that
+    fails four."""
+    from paper_2606_17787_amd.sched import Scheduler
+    rng = np.random.default_rng(12)
+    nw, nreq = 64, 100_000
+    row = 131072  # Llama-3-8B-shaped token row, bytes
+    s = Scheduler([80 * 10**9] * nw, 26e9, 1.0)
+    for w in range(nw):
+        s.set_worker(w, float(rng.random() * 0.5), int(rng.integers(0, 8)),
+                     int(rng.integers(16, 64)))
+    serving = rng.integers(0, nw, nreq)
+    foot = rng.integers(2048, 16385, nreq) * row  # from max context
+    t0 = time.perf_counter()
+    live, protected = [], 0
+    for r in range(nreq):
+        protected += s.place(r, int(serving[r]), int(foot[r])) >= 0
+        live.append(r)
+        if len(live) > 4000:  # requests complete: keep 4000 active
+            s.release(live.pop(0))
+    t_place = time.perf_counter() - t0
+    for r in live:
+        s.set_persisted(r, int(rng.integers(0, foot[r])))
+    t0 = time.perf_counter()
+    one = s.recover([5])
+    t_one = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    four = s.recover([9, 17, 33, 60])
+    t_four = time.perf_counter() - t0
+    s.close()
+    return {"workers": nw, "placements": nreq, "active_requests": 4000,
+            "placed_with_holder": int(protected),
+            "place_us": t_place / nreq * 1e6,
+            "recover_1_failure_interrupted": len(one),
+            "recover_1_failure_ms": t_one * 1e3,
+            "recover_1_failure_reuse": sum(1 for x in one if x[2]),
+            "recover_4_failures_interrupted": len(four),
+            "recover_4_failures_ms": t_four * 1e3}
+
+
 def calibrate_copy(torch, mib):
     """A plain device-to-device copy of known size: read + write bytes are
     exactly 2 * mib MiB per launch, the scale for the FETCH_SIZE/WRITE_SIZE
@@ -833,6 +878,9 @@ def main():
     if "tags" in legs:
         say("[bench] page tags (host)")
         out["workloads"]["page-tags"] = rounded(tags_leg(W))
+    if "sched" in legs:
+        say("[bench] placement and recovery scheduling (host)")
+        out["workloads"]["scheduler"] = rounded(sched_leg())
     if "cpu" in legs:
         say("[bench] cpu baseline")
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)

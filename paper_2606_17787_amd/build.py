@@ -3,9 +3,10 @@
     python -m paper_2606_17787_amd.build
 
 compiles csrc/lumen_kv_ckpt.hip (device kernels and their host entry
-points) and csrc/lumen_page_tags.cpp (host-only page tags) with hipcc into
-paper_2606_17787_amd/liblumen_kv_ckpt.so (position-independent, C ABI from
-include/lumen_kv_ckpt.h and include/lumen_page_tags.h).
+points), csrc/lumen_page_tags.cpp (host-only page tags) and
+csrc/lumen_sched.cpp (host-only placement and recovery scheduling) with hipcc
+into paper_2606_17787_amd/liblumen_kv_ckpt.so (position-independent, C ABI
+from include/lumen_kv_ckpt.h, lumen_page_tags.h and lumen_sched.h).
 """
 from __future__ import annotations
 
@@ -17,6 +18,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "lumen_kv_ckpt.hip")
 SRC_TAGS = os.path.join(PKG, "csrc", "lumen_page_tags.cpp")
+SRC_SCHED = os.path.join(PKG, "csrc", "lumen_sched.cpp")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblumen_kv_ckpt.so")
 ARCH = "gfx950"
@@ -32,7 +34,7 @@ HIPCC_FLAGS = [
 def build(out: str = LIB, extra_flags=(), verbose: bool = False) -> str:
     hipcc = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
     cmd = [hipcc, *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, SRC, SRC_TAGS,
-           "-o", out]
+           SRC_SCHED, "-o", out]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

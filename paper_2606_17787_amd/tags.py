@@ -94,10 +94,11 @@ class TagStore:
         if not self._h:
             raise _kv.LumenError(_kv.LUMEN_ERR_INVALID_ARG,
                                  "lumen_tag_store_create")
+        self._destroy = _lib().lumen_tag_store_destroy
 
     def close(self):
-        if self._h:
-            _lib().lumen_tag_store_destroy(self._h)
+        if getattr(self, "_h", None):
+            self._destroy(self._h)
             self._h = None
 
     def __del__(self):

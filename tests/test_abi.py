@@ -43,6 +43,15 @@ def test_exports_every_page_tag_entry_point(lib):
         assert hasattr(lib, n), n
 
 
+def test_exports_every_scheduler_entry_point(lib):
+    from paper_2606_17787_amd import sched
+    names = sched.exported_names()
+    assert set(names) >= {"lumen_sched_create", "lumen_sched_place",
+                          "lumen_sched_recover", "lumen_sched_release"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
 def test_missing_library_fails_loudly(tmp_path):
     with pytest.raises(RuntimeError, match="build the HIP library"):
         kv.load_library(str(tmp_path / "absent.so"))

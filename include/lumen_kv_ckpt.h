@@ -28,6 +28,9 @@
  *           memory overlapped with the unpack
  *   validate_targets
  *           validate mode of a restore (duplicate target blocks)
+ *   draft_align
+ *           draft-state alignment of speculation-assisted recovery: truncate
+ *           the draft KV at the first token mismatch (Sec. 4.4)
  *
  * Layouts.  The cache is one allocation of elements of elem_bytes bytes
  * (2 for bf16/fp16, 1 for an 8-bit cache, 4 for fp32; always moved as raw
@@ -242,6 +245,38 @@ int lumen_kv_ckpt_validate_targets(const lumen_kv_layout *layout,
                                    int32_t bt_cols, int32_t num_reqs,
                                    void *d_workspace, void *d_marks,
                                    size_t marks_bytes, lumen_stream_t stream);
+
+/* Draft-state alignment (Sec. 4.4): after a progress update, the recovering
+ * worker's draft KV stays valid only up to the first position where its
+ * draft tokens and the authoritative committed tokens differ (compared by
+ * position, not value).  For each request r:
+ *   p = first i < min(draft_len, committed_len) with draft[i] !=
+ *       committed[i], else that minimum;
+ *   kv_len[r] <- valid = min(kv_len[r], p)          (in place);
+ *   replay[r] <- committed_len[r] - valid  (committed tokens to run through
+ *                                           the draft model again);
+ *   pages ceil(valid/bs) .. ceil(old kv_len/bs) - 1 of its table are freed:
+ *   their entries become -1 and their block ids (entries < 0 skipped) go
+ *   to d_freed in request order, then page order.
+ * *d_freed_count receives the number of freed blocks.  If it exceeds
+ * freed_cap, only the first freed_cap are listed and cleared (the others
+ * stay in their tables) and CAPACITY is recorded.  A request with negative
+ * lengths, lengths past draft_cols / committed_cols, or kv_len past
+ * bt_cols * block_size is left unchanged (replay 0) and RANGE is recorded.
+ * Layouts: d_draft [R][draft_cols], d_committed [R][committed_cols],
+ * d_block_tables [R][bt_cols] (int32, row-major); lengths [R] int32.
+ * d_workspace: a workspace of lumen_kv_ckpt_plan_workspace_bytes(R) bytes;
+ * the call starts a new error epoch there (read it with
+ * lumen_kv_ckpt_status) and the workspace holds no copy plan afterwards. */
+int lumen_kv_draft_align(const int32_t *d_draft, int32_t draft_cols,
+                         const int32_t *d_draft_len,
+                         const int32_t *d_committed, int32_t committed_cols,
+                         const int32_t *d_committed_len, int32_t *d_kv_len,
+                         int32_t *d_block_tables, int32_t bt_cols,
+                         int32_t block_size, int32_t num_reqs,
+                         int32_t *d_replay, int32_t *d_freed,
+                         int64_t freed_cap, int64_t *d_freed_count,
+                         void *d_workspace, lumen_stream_t stream);
 
 /* Synchronises `stream`, then returns and clears the workspace's error word
  * (LUMEN_OK if no device-side error was recorded since the last plan). */

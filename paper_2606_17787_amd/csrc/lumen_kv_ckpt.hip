@@ -557,6 +557,133 @@ __global__ __launch_bounds__(kBlockThreads) void validate_kernel(
   }
 }
 
+// Draft-state alignment, step 1: one wavefront per request (grid-strided)
+// finds the first position where the draft and committed tokens differ, 64
+// positions per ballot, truncates the request's KV length to it, and
+// counts the allocated table entries of the pages the shorter KV no longer
+// reaches.  Per request it leaves in the workspace the count (-1 for a
+// request with inconsistent lengths, which is left unchanged) and the page
+// span [lo, hi) packed into one int64.
+__global__ __launch_bounds__(kBlockThreads) void draft_match_kernel(
+    const int32_t *__restrict__ draft, int32_t draft_cols,
+    const int32_t *__restrict__ draft_len,
+    const int32_t *__restrict__ committed, int32_t committed_cols,
+    const int32_t *__restrict__ committed_len, int32_t *kv_len,
+    const int32_t *__restrict__ block_tables, int32_t bt_cols,
+    int32_t block_size, int32_t num_reqs, int32_t *replay, int64_t *count,
+    int64_t *span) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  const int64_t nw = int64_t(gridDim.x) * kWavesPerBlock;
+  for (int64_t r = gw; r < num_reqs; r += nw) {
+    const int32_t dl = draft_len[r], cl = committed_len[r], kl = kv_len[r];
+    if (dl < 0 || cl < 0 || kl < 0 || dl > draft_cols ||
+        cl > committed_cols || int64_t(kl) > int64_t(bt_cols) * block_size) {
+      if (lane == 0) {
+        count[r] = -1;
+        span[r] = 0;
+        replay[r] = 0;
+      }
+      continue;
+    }
+    const int32_t lim = min(dl, cl);
+    const int32_t *d = draft + r * draft_cols;
+    const int32_t *c = committed + r * committed_cols;
+    int32_t p = lim;
+    for (int32_t base = 0; base < lim; base += kWave) {
+      const int32_t i = base + lane;
+      const uint64_t m = __ballot(i < lim && d[i] != c[i]);
+      if (m) {  // wave-uniform
+        p = base + __ffsll(static_cast<unsigned long long>(m)) - 1;
+        break;
+      }
+    }
+    const int32_t valid = min(kl, p);
+    const int32_t lo = (valid + block_size - 1) / block_size;
+    const int32_t hi = (kl + block_size - 1) / block_size;
+    int64_t n = 0;
+    const int32_t *row = block_tables + r * bt_cols;
+    for (int32_t j = lo + lane; j - lane < hi; j += kWave)
+      n += __popcll(__ballot(j < hi && row[j] >= 0));
+    if (lane == 0) {
+      kv_len[r] = valid;
+      replay[r] = cl - valid;
+      count[r] = n;
+      span[r] = (int64_t(lo) << 32) | int64_t(hi);
+    }
+  }
+}
+
+// Draft-state alignment, step 2: one workgroup scans the per-request counts
+// (as the row plan does), lists the freed block ids in request order, then
+// page order, clears their table entries, and writes the status of this
+// call into the workspace's error word (a new epoch).
+__global__ __launch_bounds__(kPlanThreads) void draft_free_kernel(
+    int32_t *block_tables, int32_t bt_cols, int32_t R,
+    const int64_t *__restrict__ count, const int64_t *__restrict__ span,
+    int32_t *freed, int64_t freed_cap, int64_t *freed_count,
+    WsHeader *hdr) {
+  constexpr int kWaves = kPlanThreads / kWave;
+  __shared__ int64_t wave_sum[kWaves];
+  __shared__ int bad;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wid = tid / kWave;
+  const int32_t per = (R + kPlanThreads - 1) / kPlanThreads;
+  const int32_t lo = min(R, tid * per);
+  const int32_t hi = min(R, lo + per);
+  int64_t local = 0;
+  int my_bad = 0;
+  for (int32_t i = lo; i < hi; ++i) {
+    const int64_t n = count[i];
+    if (n < 0) my_bad = 1; else local += n;
+  }
+  int64_t x = local;
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const int64_t y = __shfl_up(x, d, kWave);
+    if (lane >= d) x += y;
+  }
+  if (lane == kWave - 1) wave_sum[wid] = x;
+  if (tid == 0) bad = 0;
+  __syncthreads();
+  if (my_bad) atomicOr(&bad, 1);
+  if (wid == 0) {
+    int64_t v = lane < kWaves ? wave_sum[lane] : 0;
+#pragma unroll
+    for (int d = 1; d < kWaves; d <<= 1) {
+      const int64_t y = __shfl_up(v, d, kWave);
+      if (lane >= d) v += y;
+    }
+    if (lane < kWaves) wave_sum[lane] = v;
+  }
+  __syncthreads();
+  int64_t off = (wid > 0 ? wave_sum[wid - 1] : 0) + x - local;  // exclusive
+  for (int32_t i = lo; i < hi; ++i) {
+    if (count[i] <= 0) continue;
+    const int32_t a = int32_t(span[i] >> 32), b = int32_t(span[i] & 0xffffffff);
+    int32_t *row = block_tables + int64_t(i) * bt_cols;
+    for (int32_t j = a; j < b; ++j) {
+      const int32_t blk = row[j];
+      if (blk < 0) continue;
+      if (off < freed_cap) {  // an entry is cleared only once it is listed
+        freed[off] = blk;
+        row[j] = -1;
+      }
+      ++off;
+    }
+  }
+  if (tid == 0) {
+    const int64_t total = wave_sum[kWaves - 1];
+    *freed_count = total;
+    hdr->total_rows = 0;  // no copy plan in the workspace any more
+    hdr->num_reqs = -1;
+    int st = bad ? LUMEN_ERR_RANGE : LUMEN_OK;
+    if (total > freed_cap) st = min(st, LUMEN_ERR_CAPACITY);
+    hdr->err = st;
+  }
+}
+
 // ------------------------------------------------------------- host side
 
 constexpr int kMaxDevices = 64;
@@ -936,6 +1063,46 @@ int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
     if (hipEventRecord(drained[j], us) != hipSuccess) return LUMEN_ERR_HIP;
   }
   return LUMEN_OK;
+}
+
+int lumen_kv_draft_align(const int32_t *d_draft, int32_t draft_cols,
+                         const int32_t *d_draft_len,
+                         const int32_t *d_committed, int32_t committed_cols,
+                         const int32_t *d_committed_len, int32_t *d_kv_len,
+                         int32_t *d_block_tables, int32_t bt_cols,
+                         int32_t block_size, int32_t num_reqs,
+                         int32_t *d_replay, int32_t *d_freed,
+                         int64_t freed_cap, int64_t *d_freed_count,
+                         void *d_workspace, lumen_stream_t stream) {
+  if (num_reqs < 0 || draft_cols < 0 || committed_cols < 0 || bt_cols < 0 ||
+      block_size < 1 || freed_cap < 0 || !d_workspace || !d_freed_count)
+    return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(d_workspace)) return LUMEN_ERR_MISALIGNED;
+  if (num_reqs > 0 &&
+      (!d_draft_len || !d_committed_len || !d_kv_len || !d_replay ||
+       (!d_draft && draft_cols > 0) || (!d_committed && committed_cols > 0) ||
+       (!d_block_tables && bt_cols > 0)))
+    return LUMEN_ERR_INVALID_ARG;
+  if (!d_freed && freed_cap > 0) return LUMEN_ERR_INVALID_ARG;
+  DeviceInfo *dev = nullptr;
+  int st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  WsView v = ws_view(d_workspace, num_reqs);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (num_reqs > 0) {
+    int64_t blocks = (int64_t(num_reqs) + kWavesPerBlock - 1) / kWavesPerBlock;
+    const int64_t cap = int64_t(dev->cus) * 8;
+    if (blocks > cap) blocks = cap;
+    hipLaunchKernelGGL(draft_match_kernel, dim3(unsigned(blocks)),
+                       dim3(kBlockThreads), 0, s, d_draft, draft_cols,
+                       d_draft_len, d_committed, committed_cols,
+                       d_committed_len, d_kv_len, d_block_tables, bt_cols,
+                       block_size, num_reqs, d_replay, v.prefix, v.first_row);
+  }
+  hipLaunchKernelGGL(draft_free_kernel, dim3(1), dim3(kPlanThreads), 0, s,
+                     d_block_tables, bt_cols, num_reqs, v.prefix, v.first_row,
+                     d_freed, freed_cap, d_freed_count, v.hdr);
+  return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
 }
 
 int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream) {

@@ -58,7 +58,8 @@ def exported_names():
     """Entry points declared in include/lumen_kv_ckpt.h."""
     with open(HEADER) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(lumen_kv_ckpt_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(lumen_kv_(?:ckpt|draft)_\w+)\s*\(",
+                                 text)))
 
 
 _LIB: Optional[ctypes.CDLL] = None
@@ -83,6 +84,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_unpack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
         "lumen_kv_ckpt_status": (ctypes.c_int, [p, p]),
         "lumen_kv_ckpt_marks_bytes": (sz, [i64]),
+        "lumen_kv_draft_align": (ctypes.c_int,
+                                 [p, i32, p, p, i32, p, p, p, i32, i32, i32,
+                                  p, p, i64, p, p, p]),
         "lumen_kv_ckpt_pack_rows": (ctypes.c_int,
                                     [lay, p, p, i32, i32, p, i64, i64, p, i64,
                                      i64, p]),
@@ -360,6 +364,44 @@ def lumen_kv_ckpt_unpack_from_host(shape, num_blocks: int,
         _dev(staging, "staging"), slot_rows, int(slots),
         _stream_handle(copy_stream), _stream_handle(unpack_stream)),
         "lumen_kv_ckpt_unpack_from_host")
+
+
+def lumen_kv_draft_align(draft: torch.Tensor, draft_len: torch.Tensor,
+                         committed: torch.Tensor,
+                         committed_len: torch.Tensor, kv_len: torch.Tensor,
+                         block_tables: torch.Tensor, block_size: int,
+                         replay: torch.Tensor, freed: torch.Tensor,
+                         freed_count: torch.Tensor, workspace: torch.Tensor,
+                         stream: Optional[torch.cuda.Stream] = None) -> None:
+    """Draft-state alignment: truncates kv_len and block_tables in place at
+    the first draft/committed mismatch of every request; replay receives
+    the committed tokens to replay, freed the freed block ids and
+    freed_count (one int64) their number."""
+    R = block_tables.shape[0] if block_tables.dim() == 2 else -1
+    for t, name in ((draft, "draft"), (committed, "committed")):
+        if t.dim() != 2 or t.shape[0] != R:
+            raise ValueError(f"{name} must be [num_reqs, cols]")
+    for t, name in ((draft_len, "draft_len"), (committed_len, "committed_len"),
+                    (kv_len, "kv_len"), (replay, "replay")):
+        if t.numel() != R:
+            raise ValueError(f"{name} must have one entry per request")
+    if freed_count.numel() < 1:
+        raise ValueError("freed_count needs one element")
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    i32 = torch.int32
+    _check(load_library().lumen_kv_draft_align(
+        _dev(draft, "draft", i32), draft.shape[1],
+        _dev(draft_len, "draft_len", i32),
+        _dev(committed, "committed", i32), committed.shape[1],
+        _dev(committed_len, "committed_len", i32),
+        _dev(kv_len, "kv_len", i32), _dev(block_tables, "block_tables", i32),
+        block_tables.shape[1], int(block_size), R,
+        _dev(replay, "replay", i32), _dev(freed, "freed", i32),
+        freed.numel(), _dev(freed_count, "freed_count", torch.int64),
+        _dev(workspace, "workspace"), _stream_handle(stream)),
+        "lumen_kv_draft_align")
 
 
 def lumen_kv_ckpt_marks_bytes(num_blocks: int) -> int:

@@ -28,7 +28,8 @@ def test_exports_every_declared_entry_point(lib):
                           "lumen_kv_ckpt_pack_rows",
                           "lumen_kv_ckpt_unpack_rows",
                           "lumen_kv_ckpt_pack_to_host",
-                          "lumen_kv_ckpt_unpack_from_host"}
+                          "lumen_kv_ckpt_unpack_from_host",
+                          "lumen_kv_draft_align"}
     for n in names:
         assert hasattr(lib, n), n
 
@@ -239,3 +240,23 @@ def test_pipeline_host_validation(lib):
         # nothing to move: no HIP call at all
         assert call(total=0, staging=None, host=None) == kv.LUMEN_OK
         assert call(R=0) == kv.LUMEN_OK
+
+
+def test_draft_align_host_validation(lib):
+    f = lib.lumen_kv_draft_align
+
+    def call(dc=8, cc=8, btc=4, bs=4, R=2, cap=10, ws=FAKE, cnt=FAKE,
+             freed=FAKE, kl=FAKE):
+        return f(FAKE, dc, FAKE, FAKE, cc, FAKE, kl, FAKE, btc, bs, R, FAKE,
+                 freed, cap, cnt, ws, None)
+
+    assert call(bs=0) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(R=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(dc=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(btc=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(cap=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ws=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(cnt=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(kl=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(freed=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ws=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED

@@ -28,6 +28,7 @@ Further legs (reported beside the headline, not part of its value):
                     every restore-burst request restored from host memory
   * page tags       host-side tag generation and longest-prefix lookups
   * scheduler       host-side Eq. 1 placement and recovery events
+  * draft-align     draft-state alignment of 1,024 mirror requests
   * cpu_baseline    the CPU oracle on a bounded sample of the decode workload,
                     on one thread and split over the host's threads
 
@@ -52,7 +53,7 @@ HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
 ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "tags", "sched",
-            "cpu")
+            "draft", "cpu")
 EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step
 
 
@@ -664,6 +665,58 @@ def sched_leg():
             "recover_4_failures_ms": t_four * 1e3}
 
 
+def draft_leg(torch, kv, reps=50):
+    """Draft-state alignment for a paired worker's batch: 1,024 mirror
+    requests with 1-4K-token histories and K = 4 draft tokens each, of
+    which a random number (0-4) were accepted before the correction; block
+    size 16.  Times lumen_kv_draft_align with HIP events."""
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(13)
+    R, K, bs = 1024, 4, 16
+    hist = rng.integers(1024, 4097, R)
+    cols = int(hist.max()) + K + 1
+    base = rng.integers(0, 128256, (R, cols)).astype(np.int32)
+    draft = base.copy()
+    committed = base.copy()
+    acc = rng.integers(0, K + 1, R)
+    for r in range(R):  # committed: history + accepted drafts + correction
+        committed[r, hist[r] + acc[r]] = -1 - int(rng.integers(0, 1000))
+    dl = (hist + K).astype(np.int32)
+    cl = (hist + acc + 1).astype(np.int32)
+    btc = -(-cols // bs)
+    bt = np.arange(R * btc, dtype=np.int32).reshape(R, btc)
+    d = {k: torch.from_numpy(v).to(dev) for k, v in dict(
+        draft=draft, committed=committed, dl=dl, cl=cl, bt=bt).items()}
+    kl0 = torch.from_numpy(dl.copy()).to(dev)
+    kl = kl0.clone()
+    tab = d["bt"].clone()
+    replay = torch.empty(R, dtype=torch.int32, device=dev)
+    freed = torch.empty(R * 2, dtype=torch.int32, device=dev)
+    cnt = torch.empty(1, dtype=torch.int64, device=dev)
+    ws = kv.new_workspace(R, dev)
+    ts = []
+    for i in range(reps + 5):
+        kl.copy_(kl0)
+        tab.copy_(d["bt"])
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        kv.lumen_kv_draft_align(d["draft"], d["dl"], d["committed"], d["cl"],
+                                kl, tab, bs, replay, freed, cnt, ws)
+        b.record()
+        b.synchronize()
+        if i >= 5:
+            ts.append(a.elapsed_time(b))
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    ok = bool((kl.cpu().numpy() == hist + acc).all()
+              and (replay.cpu().numpy() == 1).all())
+    return {"requests": R, "draft_depth": K, "block_size": bs,
+            "history_tokens_mean": float(hist.mean()),
+            "align_us_mean": float(np.mean(ts) * 1e3),
+            "align_us_median": float(np.median(ts) * 1e3),
+            "freed_blocks": int(cnt.item()), "check_ok": ok}
+
+
 def calibrate_copy(torch, mib):
     """A plain device-to-device copy of known size: read + write bytes are
     exactly 2 * mib MiB per launch, the scale for the FETCH_SIZE/WRITE_SIZE
@@ -881,6 +934,9 @@ def main():
     if "sched" in legs:
         say("[bench] placement and recovery scheduling (host)")
         out["workloads"]["scheduler"] = rounded(sched_leg())
+    if "draft" in legs:
+        say("[bench] draft-state alignment")
+        out["workloads"]["draft-align"] = rounded(draft_leg(torch, kv))
     if "cpu" in legs:
         say("[bench] cpu baseline")
         out["cpu_baseline"] = cpu_baseline(W, args.cpu_seconds)

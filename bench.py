@@ -559,6 +559,9 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
     cs, us = torch.cuda.Stream(), torch.cuda.Stream()
     ws = kv.new_workspace(1, dev)
     torch.cuda.synchronize()
+    # plain copies first: the link's rate, and the first touch of the
+    # freshly pinned buffer stays out of the timed restores
+    link = host_link_rates(torch, host, staging)
     per_ms = []
     for wv in waves:
         bt = torch.from_numpy(w.dst_block_tables[wv]).to(dev)
@@ -593,7 +596,6 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
     assert kv.lumen_kv_ckpt_status(ws2) == 0
     per_ms = np.array(per_ms)
     req_b = ctx * rb
-    link = host_link_rates(torch, host, staging)
     out["restore_from_host"] = {
         "workload": w.name, "requests": int(len(per_ms)),
         "h2d_link_GBps": link["h2d"],

@@ -729,8 +729,8 @@ __global__ __launch_bounds__(kBlockThreads) void validate_kernel(
 }
 
 // Draft-state alignment, step 1: one wavefront per request (grid-strided)
-// finds the first position where the draft and committed tokens differ, 64
-// positions per ballot, truncates the request's KV length to it, and
+// finds the first position where the draft and committed tokens differ,
+// 1024 positions per round, truncates the request's KV length to it, and
 // counts the allocated table entries of the pages the shorter KV no longer
 // reaches.  Per request it leaves in the workspace the count (-1 for a
 // request with inconsistent lengths, which is left unchanged) and the page
@@ -760,12 +760,27 @@ __global__ __launch_bounds__(kBlockThreads) void draft_match_kernel(
     const int32_t lim = min(dl, cl);
     const int32_t *d = draft + r * draft_cols;
     const int32_t *c = committed + r * committed_cols;
+    // kMatch positions per lane per round, all loads in flight together;
+    // the round's first mismatch is the minimum over the lanes.
+    constexpr int kMatch = 16;
     int32_t p = lim;
-    for (int32_t base = 0; base < lim; base += kWave) {
-      const int32_t i = base + lane;
-      const uint64_t m = __ballot(i < lim && d[i] != c[i]);
-      if (m) {  // wave-uniform
-        p = base + __ffsll(static_cast<unsigned long long>(m)) - 1;
+    for (int32_t base = 0; base < lim; base += kWave * kMatch) {
+      int32_t dv[kMatch], cv[kMatch];
+#pragma unroll
+      for (int k = 0; k < kMatch; ++k) {
+        const int32_t i = base + k * kWave + lane;
+        dv[k] = i < lim ? d[i] : 0;
+        cv[k] = i < lim ? c[i] : 0;
+      }
+      int32_t mine = INT32_MAX;
+#pragma unroll
+      for (int k = kMatch - 1; k >= 0; --k)
+        if (dv[k] != cv[k]) mine = base + k * kWave + lane;
+#pragma unroll
+      for (int off = kWave / 2; off > 0; off >>= 1)
+        mine = min(mine, __shfl_xor(mine, off, kWave));
+      if (mine != INT32_MAX) {  // wave-uniform after the reduction
+        p = mine;
         break;
       }
     }

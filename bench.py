@@ -359,11 +359,18 @@ def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
     ws = kv.new_workspace(R, dev)
     kv.lumen_kv_ckpt_plan(torch.from_numpy(s_all).to(dev),
                           torch.from_numpy(e_all).to(dev), ws)
+    bt_new = torch.from_numpy(w.dst_block_tables).to(dev)
+    # validate mode on the restore table before the unpack (timed apart)
+    marks = kv.new_marks(w.num_blocks, dev)
+    t_val = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    t_val[0].record()
+    kv.lumen_kv_ckpt_validate_targets(sh, w.num_blocks, bt_new, ws, marks)
+    t_val[1].record()
+    torch.cuda.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws) == 0
     t_un = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     t_un[0].record()
-    kv.lumen_kv_ckpt_unpack(sh, w.num_blocks, pool,
-                            torch.from_numpy(w.dst_block_tables).to(dev), ws,
-                            arena)
+    kv.lumen_kv_ckpt_unpack(sh, w.num_blocks, pool, bt_new, ws, arena)
     t_un[1].record()
     torch.cuda.synchronize()
     assert kv.lumen_kv_ckpt_status(ws) == 0
@@ -383,6 +390,9 @@ def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
                 pack_slowdown_with_d2h=with_ms / alone_ms,
                 unpack_in_place_GBps=gb(byts) / (un_ms / 1e3),
                 unpack_ms=un_ms,
+                validate_us=t_val[0].elapsed_time(t_val[1]) * 1e3,
+                validate_pages=int(sum(-(-int(x) // sh.block_size)
+                                       for x in e_all)),
                 d2h_GBps=gb(n_rows * rb) / (d2h_ms / 1e3), d2h_ms=d2h_ms,
                 d2h_bytes=n_rows * rb, d2h_spot_check_ok=ok,
                 pinned_ring=f"{ring} x {slot_bytes >> 30} GiB")

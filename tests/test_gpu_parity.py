@@ -365,3 +365,24 @@ def test_validate_workload_tables():
     w = W.c4_llama70b_tp8()
     assert gpu_validate(w.shape, w.num_blocks, w.dst_block_tables,
                         w.starts[0], w.ends[0]) == kv.LUMEN_OK
+
+
+def test_validate_with_an_empty_pool_and_no_requests():
+    shape = CacheShape(1, 1, 8, 4, NHD)
+    # no blocks at all: every written page names a block outside the pool
+    bt = np.array([[0, 1]], np.int32)
+    want = oracle.validate_targets(shape, 0, bt, [0], [5])
+    assert want == oracle.ERR_BLOCK_ID
+    ws = kv.new_workspace(1, dev())
+    kv.lumen_kv_ckpt_plan(h2d(np.array([0], np.int32)),
+                          h2d(np.array([5], np.int32)), ws)
+    marks = torch.empty(16, dtype=torch.uint8, device=dev())
+    kv.lumen_kv_ckpt_validate_targets(shape, 0, h2d(bt), ws, marks)
+    assert kv.lumen_kv_ckpt_status(ws) == want
+    # no requests: nothing is checked, the status stays OK
+    ws0 = kv.new_workspace(0, dev())
+    e = torch.zeros(0, dtype=torch.int32, device=dev())
+    kv.lumen_kv_ckpt_plan(e, e, ws0)
+    kv.lumen_kv_ckpt_validate_targets(shape, 8, e.view(0, 2), ws0,
+                                      kv.new_marks(8, dev()))
+    assert kv.lumen_kv_ckpt_status(ws0) == 0

@@ -301,3 +301,79 @@ def test_page_tags_drive_the_restore_of_a_cut_stream():
             us.synchronize()
             assert kv.lumen_kv_ckpt_status(ws1, stream=us) == 0
         assert np.array_equal(d2h_words(d_dst, 2), want), cut
+
+
+def test_pipeline_and_row_range_errors_match_oracle():
+    """A block-table entry outside the pool, seen through a chunked pack,
+    the host pipelines and a row-range unpack, reports the oracle's code;
+    the other rows are still copied where the code allows."""
+    shape = SHAPES[0]
+    nb, bt, bt2, s, e, src, dst = case(shape, 99, R=7, max_tok=60)
+    total = int((e - s).sum())
+    assert total > 10
+    # poison a page that some token reads
+    r = int(np.argmax(e - s))
+    bad = bt.copy()
+    bad[r, s[r] // shape.block_size] = nb + 3
+    st_o, _ = oracle.pack(shape, nb, src, bad, s, e)
+    assert st_o == oracle.ERR_BLOCK_ID
+    rb = shape.token_row_bytes
+    d_src, d_bad = h2d(src), h2d(bad)
+    d_s, d_e = h2d(s), h2d(e)
+    torch.cuda.synchronize()
+    # chunked pack through windows
+    ws = planned(s, e)
+    for lo in range(0, total, 9):
+        win = window(shape, 9)
+        kv.lumen_kv_ckpt_pack_rows(shape, nb, d_src, d_bad, ws, lo, lo + 9,
+                                   win, ckpt_first_row=lo)
+    assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_ERR_BLOCK_ID
+    # the pipeline to host memory
+    staging = torch.empty(2 * 8 * rb, dtype=torch.uint8, device=dev())
+    host = torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True)
+    ps, cs = torch.cuda.Stream(), torch.cuda.Stream()
+    ws2 = kv.new_workspace(len(s), dev())
+    torch.cuda.synchronize()
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws2, stream=ps)
+    kv.lumen_kv_ckpt_pack_to_host(shape, nb, d_src, d_bad, ws2, total,
+                                  staging, 2, host, pack_stream=ps,
+                                  copy_stream=cs)
+    cs.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws2, stream=ps) == kv.LUMEN_ERR_BLOCK_ID
+    # the restore pipeline into a table with the same bad entry
+    st_u = oracle.unpack(shape, nb, dst.copy(), bad, s, e,
+                         np.zeros((total, shape.token_row_elems), np.uint16))
+    assert st_u == oracle.ERR_BLOCK_ID
+    d_dst = h2d(dst)
+    us = torch.cuda.Stream()
+    ws3 = kv.new_workspace(len(s), dev())
+    torch.cuda.synchronize()
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws3, stream=us)
+    kv.lumen_kv_ckpt_unpack_from_host(shape, nb, d_dst, d_bad, ws3, total,
+                                      host, staging, 2, copy_stream=cs,
+                                      unpack_stream=us)
+    us.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws3, stream=us) == kv.LUMEN_ERR_BLOCK_ID
+
+
+def test_pipeline_rejects_misused_buffers():
+    shape = SHAPES[0]
+    nb, bt, _, s, e, src, _ = case(shape, 3, R=3, max_tok=30)
+    total = int((e - s).sum())
+    rb = shape.token_row_bytes
+    ws = planned(s, e)
+    small_host = torch.zeros(total * rb - 16, dtype=torch.uint8,
+                             pin_memory=True)
+    staging = torch.empty(2 * 4 * rb, dtype=torch.uint8, device=dev())
+    with pytest.raises(ValueError):   # host copy smaller than the rows
+        kv.lumen_kv_ckpt_pack_to_host(shape, nb, h2d(src), h2d(bt), ws,
+                                      total, staging, 2, small_host)
+    with pytest.raises(ValueError):   # staging not whole rows per slot
+        kv.lumen_kv_ckpt_pack_to_host(
+            shape, nb, h2d(src), h2d(bt), ws, total,
+            torch.empty(2 * 4 * rb + 16, dtype=torch.uint8, device=dev()),
+            2, torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True))
+    with pytest.raises(ValueError):   # host tensor on the device
+        kv.lumen_kv_ckpt_pack_to_host(
+            shape, nb, h2d(src), h2d(bt), ws, total, staging, 2,
+            torch.zeros(total * rb, dtype=torch.uint8, device=dev()))

@@ -239,6 +239,25 @@ def restore_leg(torch, kv, W):
         wave_stats.append(dict(requests=len(wv), tokens=nrows, ms=round(t, 3),
                                GBps=round(gb(byts) / (t / 1e3), 1)))
         per_req_ms += [t * float(ctx[r]) / nrows for r in wv]
+    # per-request launches: each request of the last wave restored by its
+    # own plan + unpack (median over the wave)
+    wv = waves[-1]
+    bt = torch.from_numpy(w.dst_block_tables[wv]).to(dev)
+    s_w = torch.from_numpy(w.starts[0][wv]).to(dev)
+    e_w = torch.from_numpy(w.ends[0][wv]).to(dev)
+    ws1 = kv.new_workspace(1, dev)
+    single_ms = []
+    for i in range(len(wv)):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        kv.lumen_kv_ckpt_plan(s_w[i:i + 1], e_w[i:i + 1], ws1)
+        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, pool, bt[i:i + 1], ws1,
+                                ck[:int(ctx[wv[i]]) * row_elems])
+        b.record()
+        b.synchronize()
+        single_ms.append(a.elapsed_time(b))
+    assert kv.lumen_kv_ckpt_status(ws1) == 0
     del pool, ck
     torch.cuda.empty_cache()
     tot_ms = sum(x["ms"] for x in wave_stats)
@@ -246,6 +265,8 @@ def restore_leg(torch, kv, W):
     return dict(workload=w.name, requests=w.num_reqs,
                 restore_ms_per_request=tot_ms / w.num_reqs,
                 restore_ms_per_request_median=float(np.median(per_req_ms)),
+                single_request_launch_ms_median=float(np.median(single_ms)),
+                single_request_launches=len(single_ms),
                 unpack_GBps=gb(tot_b) / (tot_ms / 1e3),
                 mean_request_GB=gb(float(ctx.mean()) * sh.token_row_bytes),
                 waves=wave_stats)
@@ -839,6 +860,14 @@ def cpu_baseline(W, seconds):
 
     one, n1, b1 = run(1, seconds / 2)
     threads = cpu_threads()
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     many, n2, b2 = run(threads, seconds / 2)
     return {"value": round(many, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle",
@@ -846,6 +875,7 @@ def cpu_baseline(W, seconds):
                       f"Llama-3-8B-shaped workload ({gb(b2):.2f} GB read+"
                       "written) from a compact host pool of the blocks those "
                       f"steps read, requests split over {threads} threads",
+            "cpu_model": model,
             "single_thread_value": round(one, 4),
             "single_thread_sample": f"decode steps 0..{n1 - 1} "
                                     f"({gb(b1):.2f} GB)"}

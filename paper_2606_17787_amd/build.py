@@ -3,10 +3,12 @@
     python -m paper_2606_17787_amd.build
 
 compiles csrc/lumen_kv_ckpt.hip (device kernels and their host entry
-points), csrc/lumen_page_tags.cpp (host-only page tags) and
-csrc/lumen_sched.cpp (host-only placement and recovery scheduling) with hipcc
-into paper_2606_17787_amd/liblumen_kv_ckpt.so (position-independent, C ABI
-from include/lumen_kv_ckpt.h, lumen_page_tags.h and lumen_sched.h).
+points) and the host-only csrc/lumen_page_tags.cpp (page tags),
+csrc/lumen_sched.cpp (placement and recovery scheduling) and
+csrc/lumen_progress.cpp (checkpoint progress) with hipcc into
+paper_2606_17787_amd/liblumen_kv_ckpt.so (position-independent, C ABI from
+include/lumen_kv_ckpt.h, lumen_page_tags.h, lumen_sched.h and
+lumen_progress.h).
 """
 from __future__ import annotations
 
@@ -19,6 +21,7 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "lumen_kv_ckpt.hip")
 SRC_TAGS = os.path.join(PKG, "csrc", "lumen_page_tags.cpp")
 SRC_SCHED = os.path.join(PKG, "csrc", "lumen_sched.cpp")
+SRC_PROGRESS = os.path.join(PKG, "csrc", "lumen_progress.cpp")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "liblumen_kv_ckpt.so")
 ARCH = "gfx950"
@@ -34,7 +37,7 @@ HIPCC_FLAGS = [
 def build(out: str = LIB, extra_flags=(), verbose: bool = False) -> str:
     hipcc = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "bin", "hipcc")
     cmd = [hipcc, *HIPCC_FLAGS, *extra_flags, "-I", INCLUDE, SRC, SRC_TAGS,
-           SRC_SCHED, "-o", out]
+           SRC_SCHED, SRC_PROGRESS, "-o", out]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

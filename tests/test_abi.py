@@ -53,6 +53,15 @@ def test_exports_every_scheduler_entry_point(lib):
         assert hasattr(lib, n), n
 
 
+def test_exports_every_progress_entry_point(lib):
+    from paper_2606_17787_amd import progress
+    names = progress.exported_names()
+    assert set(names) >= {"lumen_progress_create", "lumen_progress_ranges",
+                          "lumen_progress_sent", "lumen_progress_release"}
+    for n in names:
+        assert hasattr(lib, n), n
+
+
 def test_missing_library_fails_loudly(tmp_path):
     with pytest.raises(RuntimeError, match="build the HIP library"):
         kv.load_library(str(tmp_path / "absent.so"))

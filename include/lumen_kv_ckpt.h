@@ -192,7 +192,17 @@ int lumen_kv_ckpt_unpack_rows(const lumen_kv_layout *layout, void *d_cache,
  * caller knows it: the sum of its ranges).  Both streams must differ from
  * the serving stream for the work to stay off it.  Returns after enqueuing;
  * the copies are complete once copy_stream has drained.  1 <= slots <= 64,
- * slot_rows >= 1 (INVALID_ARG).  Device errors go to the workspace word. */
+ * slot_rows >= 1 (INVALID_ARG).  Device errors go to the workspace word.
+ *
+ * Reuse of the staging ring.  The ring is busy until the last stream that
+ * touches it (copy_stream here, unpack_stream in the restore) has passed
+ * this call's work.  A later pipeline call (either direction) with the same
+ * d_staging pointer on the same device waits for that on its own, outside
+ * graph capture: its first stream to write the ring waits on an event the
+ * earlier call recorded.  The library remembers the last 16 rings per
+ * device.  The caller orders every other reuse: a ring reached through a
+ * different pointer (an overlapping view), a 17th ring, or a call being
+ * captured into a graph. */
 int lumen_kv_ckpt_pack_to_host(const lumen_kv_layout *layout,
                                const void *d_cache,
                                const int32_t *d_block_tables, int32_t bt_cols,
@@ -208,8 +218,8 @@ int lumen_kv_ckpt_pack_to_host(const lumen_kv_layout *layout,
  * writes them) are copied into the staging ring on copy_stream, and each is
  * unpacked on unpack_stream as soon as it has arrived; a slot is refilled
  * only after its previous unpack.  Same plan, total_rows and slot rules as
- * lumen_kv_ckpt_pack_to_host; the restore is complete once unpack_stream
- * has drained. */
+ * lumen_kv_ckpt_pack_to_host, and the same reuse rule for the ring; the
+ * restore is complete once unpack_stream has drained. */
 int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
                                    void *d_cache,
                                    const int32_t *d_block_tables,

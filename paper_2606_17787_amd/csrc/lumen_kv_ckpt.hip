@@ -1,7 +1,9 @@
 // Paged KV-cache checkpoint pack / restore unpack for MI355X (gfx950).
 //
 // The operations and layouts are specified in include/lumen_kv_ckpt.h.  This
-// file holds the three kernels (row plan, gather, scatter) and the C ABI.
+// file holds the kernels (row plan, token-major gather and scatter,
+// page-major gather, restore-target validation, draft-state alignment), the
+// staging pipelines to and from pinned host memory, and the C ABI.
 //
 // Work decomposition.  A checkpoint is a sequence of token rows, each
 // [L][2][H][D] elements of E bytes (E = 1, 2 or 4; the copy moves raw bits
@@ -874,6 +876,7 @@ __global__ __launch_bounds__(kPlanThreads) void draft_free_kernel(
 
 constexpr int kMaxDevices = 64;
 constexpr int32_t kMaxSlots = 64;  // ring slots of a staging pipeline
+constexpr size_t kMaxRings = 16;   // staging rings remembered per device
 
 struct DeviceInfo {
   std::once_flag once;
@@ -886,6 +889,17 @@ struct DeviceInfo {
   // the same event.
   std::mutex pipe_mu;
   std::vector<hipEvent_t> pipe_events;
+  // Staging rings of recent pipeline calls (pipe_mu held): per ring, an
+  // event recorded on the stream that last read or wrote it, once that
+  // call's work on the ring has been enqueued.  The next call on the same
+  // ring orders its first use after that event.
+  struct Ring {
+    const void *staging = nullptr;
+    hipEvent_t idle = nullptr;
+    bool recorded = false;
+  };
+  std::vector<Ring> rings;
+  size_t ring_next = 0;  // entry reused once kMaxRings are known
 };
 DeviceInfo g_dev[kMaxDevices];
 
@@ -1072,6 +1086,63 @@ int pipe_events(DeviceInfo *dev, size_t n) {
   return LUMEN_OK;
 }
 
+// The entry of staging ring `staging`, created (or the oldest entry
+// recycled) on first use; pipe_mu held.
+int ring_entry(DeviceInfo *dev, const void *staging, DeviceInfo::Ring **out) {
+  for (auto &r : dev->rings)
+    if (r.staging == staging) {
+      *out = &r;
+      return LUMEN_OK;
+    }
+  DeviceInfo::Ring *r = nullptr;
+  if (dev->rings.size() < kMaxRings) {
+    dev->rings.reserve(kMaxRings);  // entries never move
+    hipEvent_t ev = nullptr;
+    if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess)
+      return LUMEN_ERR_HIP;
+    dev->rings.push_back(DeviceInfo::Ring{});
+    r = &dev->rings.back();
+    r->idle = ev;
+  } else {
+    r = &dev->rings[dev->ring_next];
+    dev->ring_next = (dev->ring_next + 1) % kMaxRings;
+  }
+  r->staging = staging;
+  r->recorded = false;
+  *out = r;
+  return LUMEN_OK;
+}
+
+// Start of a staging pipeline on `first` (the stream that writes the ring
+// first): outside graph capture, wait until the previous pipeline call on
+// the same ring has finished with it.  Sets *ring to the entry to record at
+// the end, or to null while `first` is being captured (a captured graph
+// cannot wait on work outside it; its launches are ordered by the stream
+// they are launched on).
+int ring_acquire(DeviceInfo *dev, const void *staging, hipStream_t first,
+                 DeviceInfo::Ring **ring) {
+  *ring = nullptr;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(first, &cap) != hipSuccess) return LUMEN_ERR_HIP;
+  if (cap != hipStreamCaptureStatusNone) return LUMEN_OK;
+  DeviceInfo::Ring *r = nullptr;
+  const int st = ring_entry(dev, staging, &r);
+  if (st != LUMEN_OK) return st;
+  if (r->recorded && hipStreamWaitEvent(first, r->idle, 0) != hipSuccess)
+    return LUMEN_ERR_HIP;
+  *ring = r;
+  return LUMEN_OK;
+}
+
+// End of a staging pipeline: `last` is the stream whose work finishes the
+// ring's use (the copies of pack_to_host, the unpacks of unpack_from_host).
+int ring_release(DeviceInfo::Ring *ring, hipStream_t last) {
+  if (!ring) return LUMEN_OK;
+  if (hipEventRecord(ring->idle, last) != hipSuccess) return LUMEN_ERR_HIP;
+  ring->recorded = true;
+  return LUMEN_OK;
+}
+
 // Host-side checks shared by the two staging pipelines.
 int check_pipeline(const lumen_kv_layout *lay, int32_t num_reqs,
                    const void *ws, int64_t total_rows, const void *staging,
@@ -1219,6 +1290,9 @@ int lumen_kv_ckpt_pack_to_host(const lumen_kv_layout *layout,
   if (st != LUMEN_OK) return st;
   hipEvent_t *packed = dev->pipe_events.data();
   hipEvent_t *copied = packed + slots;
+  DeviceInfo::Ring *ring = nullptr;
+  st = ring_acquire(dev, d_staging, ps, &ring);
+  if (st != LUMEN_OK) return st;
   for (int64_t c = 0, lo = 0; lo < total_rows; ++c, lo += slot_rows) {
     const int64_t hi = lo + slot_rows < total_rows ? lo + slot_rows : total_rows;
     const int32_t j = int32_t(c % slots);
@@ -1237,7 +1311,7 @@ int lumen_kv_ckpt_pack_to_host(const lumen_kv_layout *layout,
         hipEventRecord(copied[j], cs) != hipSuccess)
       return LUMEN_ERR_HIP;
   }
-  return LUMEN_OK;
+  return ring_release(ring, cs);
 }
 
 int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
@@ -1265,6 +1339,9 @@ int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
   if (st != LUMEN_OK) return st;
   hipEvent_t *staged = dev->pipe_events.data();
   hipEvent_t *drained = staged + slots;
+  DeviceInfo::Ring *ring = nullptr;
+  st = ring_acquire(dev, d_staging, cs, &ring);
+  if (st != LUMEN_OK) return st;
   for (int64_t c = 0, lo = 0; lo < total_rows; ++c, lo += slot_rows) {
     const int64_t hi = lo + slot_rows < total_rows ? lo + slot_rows : total_rows;
     const int32_t j = int32_t(c % slots);
@@ -1283,7 +1360,7 @@ int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
     if (st != LUMEN_OK) return st;
     if (hipEventRecord(drained[j], us) != hipSuccess) return LUMEN_ERR_HIP;
   }
-  return LUMEN_OK;
+  return ring_release(ring, us);
 }
 
 int lumen_kv_draft_align(const int32_t *d_draft, int32_t draft_cols,

@@ -377,3 +377,70 @@ def test_pipeline_rejects_misused_buffers():
         kv.lumen_kv_ckpt_pack_to_host(
             shape, nb, h2d(src), h2d(bt), ws, total, staging, 2,
             torch.zeros(total * rb, dtype=torch.uint8, device=dev()))
+
+
+def test_back_to_back_pipelines_share_one_ring():
+    """Pipeline calls issued one after another on one staging ring, with no
+    host synchronisation between them and nothing else ordering them:
+    eight checkpoints of different plans to eight host buffers, then three
+    restores from host buffers prepared beforehand, on two other streams.
+    Each call's first write into the ring waits for the previous call on
+    that ring, so every host copy and every restored pool equals the
+    oracle's."""
+    shape = CacheShape(4, 8, 128, 16, NHD)  # 16 KiB rows
+    rb = shape.token_row_bytes
+    rng = np.random.default_rng(404)
+    R, max_tok, bs = 16, 256, shape.block_size
+    cols = max_tok // bs
+    nb = R * cols + 9
+    bt = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    bt2 = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    src = W.random_words(rng, shape.pool_elems(nb), 2)
+    dst = W.random_words(rng, shape.pool_elems(nb), 2)
+    steps = []
+    for _ in range(8):
+        s = rng.integers(0, max_tok // 2, R).astype(np.int32)
+        e = np.minimum(s + rng.integers(40, 200, R), max_tok).astype(np.int32)
+        steps.append((s, e, int((e - s).sum())))
+    wants = []
+    for s, e, _ in steps:
+        st, want = oracle.pack(shape, nb, src, bt, s, e)
+        assert st == 0
+        wants.append(want)
+    restores = (0, 3, 6)
+    # everything allocated and filled before the first call
+    d_src, d_bt, d_bt2 = h2d(src), h2d(bt), h2d(bt2)
+    ranges = [(h2d(s), h2d(e)) for s, e, _ in steps]
+    slots, slot_rows = 2, 96  # 3 MiB ring, about 20 chunks per call
+    staging = torch.empty(slots * slot_rows * rb, dtype=torch.uint8,
+                          device=dev())
+    hosts = [torch.zeros(t * rb, dtype=torch.uint8, pin_memory=True)
+             for _, _, t in steps]
+    wss = [kv.new_workspace(R, dev()) for _ in steps]
+    sources = [pinned(wants[k]) for k in restores]
+    pools = [h2d(dst) for _ in restores]
+    wss_r = [kv.new_workspace(R, dev()) for _ in restores]
+    ps, cs = torch.cuda.Stream(), torch.cuda.Stream()
+    cs2, us2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for (d_s, d_e), (_, _, total), host, ws in zip(ranges, steps, hosts, wss):
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws, stream=ps)
+        kv.lumen_kv_ckpt_pack_to_host(shape, nb, d_src, d_bt, ws, total,
+                                      staging, slots, host, pack_stream=ps,
+                                      copy_stream=cs)
+    for k, host, d_pool, ws in zip(restores, sources, pools, wss_r):
+        kv.lumen_kv_ckpt_plan(ranges[k][0], ranges[k][1], ws, stream=us2)
+        kv.lumen_kv_ckpt_unpack_from_host(shape, nb, d_pool, d_bt2, ws,
+                                          steps[k][2], host, staging, slots,
+                                          copy_stream=cs2, unpack_stream=us2)
+    torch.cuda.synchronize()
+    for i, (host, want, ws) in enumerate(zip(hosts, wants, wss)):
+        assert kv.lumen_kv_ckpt_status(ws, stream=ps) == 0
+        got = host.numpy().view(np.uint16).reshape(want.shape)
+        assert np.array_equal(got, want), i
+    for k, d_pool, ws in zip(restores, pools, wss_r):
+        assert kv.lumen_kv_ckpt_status(ws, stream=us2) == 0
+        want_dst = dst.copy()
+        assert oracle.unpack(shape, nb, want_dst, bt2, steps[k][0],
+                             steps[k][1], wants[k]) == 0
+        assert np.array_equal(d2h_words(d_pool, 2), want_dst), k

@@ -277,7 +277,9 @@ def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
     one launch; the same pack in request chunks, alone and with each chunk's
     rows streamed to a ring of pinned host buffers on a side stream as soon
     as the chunk is packed (the chunked pack's slowdown under the concurrent
-    D2H); then an in-place unpack under a fresh permutation."""
+    D2H); the whole checkpoint packed straight into that pinned ring with no
+    device arena (direct mode); then an in-place unpack under a fresh
+    permutation."""
     dev = torch.device("cuda:0")
     w = W.c4_llama70b_tp8()
     sh = w.shape
@@ -377,6 +379,35 @@ def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
         ok &= bool(torch.equal(host[j][:k], arena16[off:off + k].cpu()))
     for ws in wss:
         assert kv.lumen_kv_ckpt_status(ws) == 0
+    # The whole checkpoint straight from the paged cache into the pinned
+    # ring, window by window, with no device arena: the gather writes host
+    # memory itself (one plan, one direct pack per 2 GiB slot).
+    slot_rows = slot_bytes // rb
+    views = [h[:slot_rows * rb // 2] for h in host]
+    slot_free = [None] * ring
+    t_dir = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    kv.lumen_kv_ckpt_plan(s_dev, e_dev, ws_all)
+    t_dir[0].record()
+    last = None
+    for c, lo in enumerate(range(0, n_rows, slot_rows)):
+        j = c % ring
+        if slot_free[j] is not None:
+            slot_free[j].synchronize()  # the host drains the slot
+        kv.lumen_kv_ckpt_pack_to_host_direct(
+            sh, w.num_blocks, pool, bt, ws_all, views[j], row_begin=lo,
+            row_end=lo + slot_rows, ckpt_first_row=lo)
+        ev = torch.cuda.Event()
+        ev.record()
+        slot_free[j] = ev
+        last = (lo, j)
+    t_dir[1].record()
+    torch.cuda.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws_all) == 0
+    lo, j = last
+    k = min(n_rows - lo, 64) * rb // 2
+    direct_ok = bool(torch.equal(host[j][:k],
+                                 arena16[lo * rb // 2:lo * rb // 2 + k].cpu()))
+    direct_ms = t_dir[0].elapsed_time(t_dir[1])
     ws = kv.new_workspace(R, dev)
     kv.lumen_kv_ckpt_plan(torch.from_numpy(s_all).to(dev),
                           torch.from_numpy(e_all).to(dev), ws)
@@ -416,7 +447,11 @@ def tp8_leg(torch, kv, W, chunks=8, slot_bytes=2 << 30, ring=4):
                                        for x in e_all)),
                 d2h_GBps=gb(n_rows * rb) / (d2h_ms / 1e3), d2h_ms=d2h_ms,
                 d2h_bytes=n_rows * rb, d2h_spot_check_ok=ok,
-                pinned_ring=f"{ring} x {slot_bytes >> 30} GiB")
+                pinned_ring=f"{ring} x {slot_bytes >> 30} GiB",
+                checkpoint_direct_to_host_GBps=gb(n_rows * rb)
+                / (direct_ms / 1e3),
+                checkpoint_direct_to_host_ms=direct_ms,
+                checkpoint_direct_spot_check_ok=direct_ok)
 
 
 def host_link_rates(torch, host, dev_buf, reps=3):
@@ -488,6 +523,9 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
     torch.cuda.synchronize()
 
     def decode_loop(ckpt):
+        """ckpt: None (decode alone), "ring" (pack_to_host through the
+        staging ring and the copy engine) or "direct" (the gather writes
+        pinned host memory itself)."""
         evs = [(torch.cuda.Event(enable_timing=True),
                 torch.cuda.Event(enable_timing=True))
                for _ in range(decode_steps)]
@@ -504,23 +542,29 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
                 k, j = i % S, i % host_slots
                 if done[j] is not None:
                     done[j].synchronize()  # the host drains slot j
+                last = copy_s if ckpt == "ring" else pack_s
                 if i == 0:
-                    c0.record(copy_s)
+                    c0.record(last)
                 issued = torch.cuda.Event(enable_timing=True)
                 issued.record(pack_s)
                 kv.lumen_kv_ckpt_plan(starts[k], ends[k], wss[j],
                                       stream=pack_s)
-                kv.lumen_kv_ckpt_pack_to_host(
-                    sh, w.num_blocks, src, bt, wss[j], int(rows[k]), staging,
-                    ring_slots, hosts[j], pack_stream=pack_s,
-                    copy_stream=copy_s)
+                if ckpt == "ring":
+                    kv.lumen_kv_ckpt_pack_to_host(
+                        sh, w.num_blocks, src, bt, wss[j], int(rows[k]),
+                        staging, ring_slots, hosts[j], pack_stream=pack_s,
+                        copy_stream=copy_s)
+                else:
+                    kv.lumen_kv_ckpt_pack_to_host_direct(
+                        sh, w.num_blocks, src, bt, wss[j], hosts[j],
+                        stream=pack_s)
                 ev = torch.cuda.Event(enable_timing=True)
-                ev.record(copy_s)
+                ev.record(last)
                 done[j] = ev
                 lat.append((issued, ev, int(rows[k])))
         t_issue = time.perf_counter() - t0
         if ckpt:
-            c1.record(copy_s)
+            c1.record(copy_s if ckpt == "ring" else pack_s)
         torch.cuda.synchronize()
         t_all = time.perf_counter() - t0
         ms = np.array([a.elapsed_time(b) for a, b in evs])
@@ -539,40 +583,54 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
                                               np.float64)
         return res
 
-    decode_loop(False)  # warm-up
-    alone = decode_loop(False)
-    withc = decode_loop(True)
-    # the last step's host copy against the device rows of that step
-    k = (decode_steps - 1) % S
-    j = (decode_steps - 1) % host_slots
-    ws = kv.new_workspace(w.num_reqs, dev)
-    kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws)
-    back = torch.empty(int(rows[k]) * rb, dtype=torch.uint8, device=dev)
-    kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws,
-                          back.view(torch.bfloat16))
-    ok = bool(torch.equal(back.cpu(), hosts[j][:back.numel()]))
-    assert kv.lumen_kv_ckpt_status(ws) == 0
+    def last_step_ok():
+        """The last step's host copy against the device rows of that step."""
+        k = (decode_steps - 1) % S
+        j = (decode_steps - 1) % host_slots
+        ws = kv.new_workspace(w.num_reqs, dev)
+        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws)
+        back = torch.empty(int(rows[k]) * rb, dtype=torch.uint8, device=dev)
+        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws,
+                              back.view(torch.bfloat16))
+        ok = bool(torch.equal(back.cpu(), hosts[j][:back.numel()]))
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+        for h in hosts:
+            h.zero_()
+        return ok
+
+    decode_loop(None)  # warm-up
+    alone = decode_loop(None)
     decode_GBps = gb(kv_view.numel() * 2) / (alone["decode_ms_mean"] / 1e3)
-    out["decode_with_checkpoint"] = {
-        "workload": w.name, "decode_steps": decode_steps,
-        "decode_standin": "one HBM-bound pass over the KV of the batch "
-                          f"({gb(kv_view.numel() * 2):.1f} GB) per step",
-        "decode_standin_GBps": decode_GBps,
-        "decode_ms_alone": alone["decode_ms_mean"],
-        "decode_ms_with_checkpoint": withc["decode_ms_mean"],
-        "decode_slowdown": withc["decode_ms_mean"] / alone["decode_ms_mean"],
-        "wall_ms_alone": alone["wall_ms"],
-        "wall_ms_with_checkpoint": withc["wall_ms"],
-        "checkpoint_GB": gb(withc["ckpt_bytes"]),
-        "checkpoint_latency_ms_mean": float(withc["ckpt_latency_ms"].mean()),
-        "checkpoint_latency_ms_max": float(withc["ckpt_latency_ms"].max()),
-        "checkpoint_step_GBps": gb(withc["ckpt_step_bytes"].sum())
-        / (withc["ckpt_latency_ms"].sum() / 1e3),
-        "d2h_link_GBps": link["d2h"],
-        "staging_ring": f"{ring_slots} x {slot_rows} rows "
-                        f"({ring_slots * slot_rows * rb / 2**20:.0f} MiB)",
-        "host_copy_ok": ok}
-    del src, kv_view, staging, hosts, back
+    for mode in ("ring", "direct"):
+        withc = decode_loop(mode)
+        ok = last_step_ok()
+        key = ("decode_with_checkpoint" if mode == "ring"
+               else "decode_with_checkpoint_direct")
+        out[key] = {
+            "workload": w.name, "decode_steps": decode_steps,
+            "decode_standin": "one HBM-bound pass over the KV of the batch "
+                              f"({gb(kv_view.numel() * 2):.1f} GB) per step",
+            "decode_standin_GBps": decode_GBps,
+            "decode_ms_alone": alone["decode_ms_mean"],
+            "decode_ms_with_checkpoint": withc["decode_ms_mean"],
+            "decode_slowdown": withc["decode_ms_mean"]
+            / alone["decode_ms_mean"],
+            "wall_ms_alone": alone["wall_ms"],
+            "wall_ms_with_checkpoint": withc["wall_ms"],
+            "checkpoint_GB": gb(withc["ckpt_bytes"]),
+            "checkpoint_latency_ms_mean":
+                float(withc["ckpt_latency_ms"].mean()),
+            "checkpoint_latency_ms_max":
+                float(withc["ckpt_latency_ms"].max()),
+            "checkpoint_step_GBps": gb(withc["ckpt_step_bytes"].sum())
+            / (withc["ckpt_latency_ms"].sum() / 1e3),
+            "d2h_link_GBps": link["d2h"],
+            "path": (f"staging ring {ring_slots} x {slot_rows} rows "
+                     f"({ring_slots * slot_rows * rb / 2**20:.0f} MiB) "
+                     "+ copy engine" if mode == "ring" else
+                     "gather writes pinned host memory (64 workgroups)"),
+            "host_copy_ok": ok}
+    del src, kv_view, staging, hosts
     torch.cuda.empty_cache()
     # --------------------------------------------------------- restore side
     w = W.c3_restore()
@@ -597,51 +655,72 @@ def staging_leg(torch, kv, W, decode_steps=40, ring_slots=2, slot_rows=1024,
     # plain copies first: the link's rate, and the first touch of the
     # freshly pinned buffer stays out of the timed restores
     link = host_link_rates(torch, host, staging)
-    per_ms = []
-    for wv in waves:
-        bt = torch.from_numpy(w.dst_block_tables[wv]).to(dev)
-        s_w = torch.from_numpy(w.starts[0][wv]).to(dev)
-        e_w = torch.from_numpy(w.ends[0][wv]).to(dev)
-        torch.cuda.synchronize()
-        for i, r in enumerate(wv):
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            bt_r = bt[i:i + 1]  # a view: nothing for the side streams to outlive
-            kv.lumen_kv_ckpt_plan(s_w[i:i + 1], e_w[i:i + 1], ws, stream=us)
-            a.record(us)
-            cs.wait_stream(us)
-            kv.lumen_kv_ckpt_unpack_from_host(
-                sh, w.dst_num_blocks, pool, bt_r, ws, int(ctx[r]), host,
-                staging, ring_slots, copy_stream=cs, unpack_stream=us)
-            b.record(us)
-            b.synchronize()
-            per_ms.append(a.elapsed_time(b))
-            assert kv.lumen_kv_ckpt_status(ws, stream=us) == 0
-    # the last request, packed back from the pool, against the host bytes
-    r = int(waves[-1][-1])
-    ws2 = kv.new_workspace(1, dev)
-    kv.lumen_kv_ckpt_plan(torch.from_numpy(w.starts[0][[r]]).to(dev),
-                          torch.from_numpy(w.ends[0][[r]]).to(dev), ws2)
-    n = min(int(ctx[r]), 512)
-    back = torch.empty(int(ctx[r]) * rb, dtype=torch.uint8, device=dev)
-    kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, pool,
-                          torch.from_numpy(w.dst_block_tables[[r]]).to(dev),
-                          ws2, back.view(torch.bfloat16))
-    ok = bool(torch.equal(back[:n * rb].cpu(), host[:n * rb]))
-    assert kv.lumen_kv_ckpt_status(ws2) == 0
-    per_ms = np.array(per_ms)
+
+    def restores(mode):
+        """Every request restored from `host`, one call each, through the
+        staging ring ("ring") or with the scatter reading host memory
+        ("direct"); ms per request."""
+        per_ms = []
+        pool.zero_()
+        for wv in waves:
+            bt = torch.from_numpy(w.dst_block_tables[wv]).to(dev)
+            s_w = torch.from_numpy(w.starts[0][wv]).to(dev)
+            e_w = torch.from_numpy(w.ends[0][wv]).to(dev)
+            torch.cuda.synchronize()
+            for i, r in enumerate(wv):
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                bt_r = bt[i:i + 1]  # a view: nothing for side streams to outlive
+                kv.lumen_kv_ckpt_plan(s_w[i:i + 1], e_w[i:i + 1], ws,
+                                      stream=us)
+                a.record(us)
+                if mode == "ring":
+                    cs.wait_stream(us)
+                    kv.lumen_kv_ckpt_unpack_from_host(
+                        sh, w.dst_num_blocks, pool, bt_r, ws, int(ctx[r]),
+                        host, staging, ring_slots, copy_stream=cs,
+                        unpack_stream=us)
+                else:
+                    kv.lumen_kv_ckpt_unpack_from_host_direct(
+                        sh, w.dst_num_blocks, pool, bt_r, ws, host,
+                        row_end=int(ctx[r]), stream=us)
+                b.record(us)
+                b.synchronize()
+                per_ms.append(a.elapsed_time(b))
+                assert kv.lumen_kv_ckpt_status(ws, stream=us) == 0
+        # the last request, packed back from the pool, against the host bytes
+        r = int(waves[-1][-1])
+        ws2 = kv.new_workspace(1, dev)
+        kv.lumen_kv_ckpt_plan(torch.from_numpy(w.starts[0][[r]]).to(dev),
+                              torch.from_numpy(w.ends[0][[r]]).to(dev), ws2)
+        n = min(int(ctx[r]), 512)
+        back = torch.empty(int(ctx[r]) * rb, dtype=torch.uint8, device=dev)
+        kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, pool,
+                              torch.from_numpy(w.dst_block_tables[[r]]).to(dev),
+                              ws2, back.view(torch.bfloat16))
+        ok = bool(torch.equal(back[:n * rb].cpu(), host[:n * rb]))
+        assert kv.lumen_kv_ckpt_status(ws2) == 0
+        return np.array(per_ms), ok
+
     req_b = ctx * rb
-    out["restore_from_host"] = {
-        "workload": w.name, "requests": int(len(per_ms)),
-        "h2d_link_GBps": link["h2d"],
-        "restore_ms_per_request": float(per_ms.mean()),
-        "restore_ms_per_request_median": float(np.median(per_ms)),
-        "h2d_GBps": gb(float(req_b.sum())) / (per_ms.sum() / 1e3),
-        "model_ms_per_request_at_26GBps": float(gb(req_b.mean()) / 26 * 1e3),
-        "staging_ring": f"{ring_slots} x {slot_rows} rows "
-                        f"({ring_slots * slot_rows * rb / 2**20:.0f} MiB)",
-        "spot_check_ok": ok}
-    del pool, host, staging, back
+    for mode in ("ring", "direct"):
+        per_ms, ok = restores(mode)
+        key = "restore_from_host" if mode == "ring" else \
+            "restore_from_host_direct"
+        out[key] = {
+            "workload": w.name, "requests": int(len(per_ms)),
+            "h2d_link_GBps": link["h2d"],
+            "restore_ms_per_request": float(per_ms.mean()),
+            "restore_ms_per_request_median": float(np.median(per_ms)),
+            "h2d_GBps": gb(float(req_b.sum())) / (per_ms.sum() / 1e3),
+            "model_ms_per_request_at_26GBps":
+                float(gb(req_b.mean()) / 26 * 1e3),
+            "path": (f"staging ring {ring_slots} x {slot_rows} rows "
+                     f"({ring_slots * slot_rows * rb / 2**20:.0f} MiB) "
+                     "+ copy engine" if mode == "ring" else
+                     "scatter reads pinned host memory (64 workgroups)"),
+            "spot_check_ok": ok}
+    del pool, host, staging
     torch.cuda.empty_cache()
     return out
 

@@ -26,6 +26,9 @@
  *           chunked pipelines through a small device staging ring: pack
  *           overlapped with the copy to host memory, and the copy from host
  *           memory overlapped with the unpack
+ *   pack_to_host_direct / unpack_from_host_direct
+ *           the gather writing, or the scatter reading, pinned host memory
+ *           itself on a small grid: no staging ring and no copy engine
  *   validate_targets
  *           validate mode of a restore (duplicate target blocks)
  *   draft_align
@@ -229,6 +232,47 @@ int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
                                    int64_t slot_rows, int32_t slots,
                                    lumen_stream_t copy_stream,
                                    lumen_stream_t unpack_stream);
+
+/* Checkpoint rows straight into pinned host memory, with no device staging
+ * (Sec. 4.2, steps 3 and 4 on one GPU): the gather kernel writes each row
+ * to host memory across the host link itself.  The same operation as
+ * lumen_kv_ckpt_pack_rows (same plan, row range and window rules; CAPACITY
+ * for rows outside the window) with d_ckpt replaced by h_ckpt, host memory
+ * of at least ckpt_rows rows that the device can address: memory from
+ * hipHostMalloc (torch's pin_memory).  Other memory is refused with
+ * INVALID_ARG before anything is enqueued.  The grid is `workgroups`
+ * workgroups of 256 threads (0: 64, which reaches the link rate on MI355X;
+ * at most 4096), so the copy holds a few CU slots rather than the chip
+ * while it waits on the link.  The rows are in host memory once `stream`
+ * has drained past the call.  One kernel, no events: the call can be
+ * captured in a graph.  h_ckpt must stay allocated until then. */
+int lumen_kv_ckpt_pack_to_host_direct(const lumen_kv_layout *layout,
+                                      const void *d_cache,
+                                      const int32_t *d_block_tables,
+                                      int32_t bt_cols, int32_t num_reqs,
+                                      void *d_workspace, int64_t row_begin,
+                                      int64_t row_end, void *h_ckpt,
+                                      int64_t ckpt_first_row,
+                                      int64_t ckpt_rows, int32_t workgroups,
+                                      lumen_stream_t stream);
+
+/* Restore straight from pinned host memory (Sec. 4.3): the scatter kernel
+ * reads each checkpoint row from host memory across the host link itself.
+ * The inverse of lumen_kv_ckpt_pack_to_host_direct; the same operation as
+ * lumen_kv_ckpt_unpack_rows with d_ckpt replaced by h_ckpt, and the same
+ * host memory, grid and ordering rules.  h_ckpt must not be written by the
+ * host until `stream` has drained past the call. */
+int lumen_kv_ckpt_unpack_from_host_direct(const lumen_kv_layout *layout,
+                                          void *d_cache,
+                                          const int32_t *d_block_tables,
+                                          int32_t bt_cols, int32_t num_reqs,
+                                          void *d_workspace,
+                                          int64_t row_begin, int64_t row_end,
+                                          const void *h_ckpt,
+                                          int64_t ckpt_first_row,
+                                          int64_t ckpt_rows,
+                                          int32_t workgroups,
+                                          lumen_stream_t stream);
 
 /* Bytes of the mark buffer lumen_kv_ckpt_validate_targets needs for a pool
  * of num_blocks blocks: one bit per block, rounded up to 16 bytes.  Returns

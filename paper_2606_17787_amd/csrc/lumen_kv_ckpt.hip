@@ -877,6 +877,12 @@ __global__ __launch_bounds__(kPlanThreads) void draft_free_kernel(
 constexpr int kMaxDevices = 64;
 constexpr int32_t kMaxSlots = 64;  // ring slots of a staging pipeline
 constexpr size_t kMaxRings = 16;   // staging rings remembered per device
+// Direct host copies: default and largest workgroup counts.  Measured on
+// MI355X, kernels moving 16-byte vectors to or from pinned host memory
+// reach the link rate (about 57 GB/s to the device, 55-56 GB/s to the
+// host) from 32-64 workgroups of 256 threads on; more only hold CU slots.
+constexpr int32_t kDirectWorkgroups = 64;
+constexpr int32_t kMaxDirectWorkgroups = 4096;
 
 struct DeviceInfo {
   std::once_flag once;
@@ -982,10 +988,14 @@ int check_layout(const lumen_kv_layout *lay) {
   return LUMEN_OK;
 }
 
+// max_waves > 0 caps the grid (a copy whose checkpoint side is host memory
+// across the host link needs a few hundred wavefronts, not the HBM grid) and
+// keeps the token-major walk, whose checkpoint accesses are sequential.
 int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
                 void *dst, const int32_t *bt, int32_t bt_cols,
                 int32_t num_reqs, void *ws, int64_t row_lo, int64_t row_hi,
-                int64_t win_first, int64_t ckpt_rows, lumen_stream_t stream) {
+                int64_t win_first, int64_t ckpt_rows, lumen_stream_t stream,
+                int64_t max_waves = 0) {
   int st = check_layout(lay);
   if (st != LUMEN_OK) return st;
   if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0) return LUMEN_ERR_INVALID_ARG;
@@ -1040,13 +1050,14 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   const int64_t max_units =
       (ckpt_rows < row_hi - row_lo ? ckpt_rows : row_hi - row_lo) *
       int64_t(lay->num_layers);
+  if (max_waves > 0 && max_waves < waves) waves = max_waves;
   if (max_units < waves) waves = max_units > 0 ? max_units : 1;
   const unsigned blocks = unsigned((waves + kWavesPerBlock - 1) / kWavesPerBlock);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint8_t *in = static_cast<const uint8_t *>(src);
   uint8_t *out = static_cast<uint8_t *>(dst);
   if (pack && !hnd && row_lo == 0 && row_hi == INT64_MAX && win_first == 0 &&
-      use_page_major(H * d_bytes)) {
+      max_waves == 0 && use_page_major(H * d_bytes)) {
     hipLaunchKernelGGL(item_scan_kernel, dim3(1), dim3(kPlanThreads), 0, s,
                        v.hdr, v.prefix, v.start, v.items, num_reqs,
                        lay->block_size);
@@ -1157,6 +1168,52 @@ int check_pipeline(const lumen_kv_layout *lay, int32_t num_reqs,
   return LUMEN_OK;
 }
 
+// Shared body of the two direct host copies: the checkpoint side is pinned
+// host memory, reached through its device address.
+int direct_copy(bool pack, const lumen_kv_layout *layout, const void *cache,
+                const void *h_ckpt, const int32_t *d_block_tables,
+                int32_t bt_cols, int32_t num_reqs, void *d_workspace,
+                int64_t row_begin, int64_t row_end, int64_t ckpt_first_row,
+                int64_t ckpt_rows, int32_t workgroups, lumen_stream_t stream) {
+  if (workgroups < 0 || workgroups > kMaxDirectWorkgroups)
+    return LUMEN_ERR_INVALID_ARG;
+  int st = check_layout(layout);
+  if (st != LUMEN_OK) return st;
+  if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0 || !d_workspace)
+    return LUMEN_ERR_INVALID_ARG;
+  if (row_begin < 0 || row_end < row_begin || ckpt_first_row < 0)
+    return LUMEN_ERR_INVALID_ARG;
+  if (num_reqs == 0 || row_end == row_begin) return LUMEN_OK;
+  void *dev_ptr = nullptr;
+  if (ckpt_rows > 0) {
+    // Memory the device cannot reach (pageable, or another process's) is
+    // refused here, before anything is enqueued: the runtime must know the
+    // pointer as pinned host memory and give its device address.
+    if (!h_ckpt) return LUMEN_ERR_INVALID_ARG;
+    hipPointerAttribute_t attr{};
+    if (hipPointerGetAttributes(&attr, h_ckpt) != hipSuccess ||
+        attr.type != hipMemoryTypeHost) {
+      (void)hipGetLastError();  // the failed query is not a sticky error
+      return LUMEN_ERR_INVALID_ARG;
+    }
+    if (hipHostGetDevicePointer(&dev_ptr, const_cast<void *>(h_ckpt), 0) !=
+            hipSuccess ||
+        !dev_ptr) {
+      (void)hipGetLastError();
+      return LUMEN_ERR_INVALID_ARG;
+    }
+  }
+  const int64_t waves =
+      int64_t(workgroups > 0 ? workgroups : kDirectWorkgroups) *
+      kWavesPerBlock;
+  return pack ? launch_copy(true, layout, cache, dev_ptr, d_block_tables,
+                            bt_cols, num_reqs, d_workspace, row_begin,
+                            row_end, ckpt_first_row, ckpt_rows, stream, waves)
+              : launch_copy(false, layout, dev_ptr, const_cast<void *>(cache),
+                            d_block_tables, bt_cols, num_reqs, d_workspace,
+                            row_begin, row_end, ckpt_first_row, ckpt_rows,
+                            stream, waves);
+}
 }  // namespace
 
 extern "C" {
@@ -1361,6 +1418,28 @@ int lumen_kv_ckpt_unpack_from_host(const lumen_kv_layout *layout,
     if (hipEventRecord(drained[j], us) != hipSuccess) return LUMEN_ERR_HIP;
   }
   return ring_release(ring, us);
+}
+
+int lumen_kv_ckpt_pack_to_host_direct(
+    const lumen_kv_layout *layout, const void *d_cache,
+    const int32_t *d_block_tables, int32_t bt_cols, int32_t num_reqs,
+    void *d_workspace, int64_t row_begin, int64_t row_end, void *h_ckpt,
+    int64_t ckpt_first_row, int64_t ckpt_rows, int32_t workgroups,
+    lumen_stream_t stream) {
+  return direct_copy(true, layout, d_cache, h_ckpt, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, row_begin, row_end,
+                     ckpt_first_row, ckpt_rows, workgroups, stream);
+}
+
+int lumen_kv_ckpt_unpack_from_host_direct(
+    const lumen_kv_layout *layout, void *d_cache,
+    const int32_t *d_block_tables, int32_t bt_cols, int32_t num_reqs,
+    void *d_workspace, int64_t row_begin, int64_t row_end,
+    const void *h_ckpt, int64_t ckpt_first_row, int64_t ckpt_rows,
+    int32_t workgroups, lumen_stream_t stream) {
+  return direct_copy(false, layout, d_cache, h_ckpt, d_block_tables, bt_cols,
+                     num_reqs, d_workspace, row_begin, row_end,
+                     ckpt_first_row, ckpt_rows, workgroups, stream);
 }
 
 int lumen_kv_draft_align(const int32_t *d_draft, int32_t draft_cols,

@@ -99,6 +99,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_unpack_from_host": (ctypes.c_int,
                                            [lay, p, p, i32, i32, p, i64, p, p,
                                             i64, i32, p, p]),
+        "lumen_kv_ckpt_pack_to_host_direct": (ctypes.c_int,
+                                              [lay, p, p, i32, i32, p, i64,
+                                               i64, p, i64, i64, i32, p]),
+        "lumen_kv_ckpt_unpack_from_host_direct": (ctypes.c_int,
+                                                  [lay, p, p, i32, i32, p,
+                                                   i64, i64, p, i64, i64,
+                                                   i32, p]),
         "lumen_kv_ckpt_validate_targets": (ctypes.c_int,
                                            [lay, p, i32, i32, p, p, sz, p]),
         "lumen_kv_ckpt_strerror": (ctypes.c_char_p, [ctypes.c_int]),
@@ -299,6 +306,72 @@ def lumen_kv_ckpt_unpack_rows(shape, num_blocks: int, cache: torch.Tensor,
     _rows_call("lumen_kv_ckpt_unpack_rows", shape, num_blocks, cache,
                block_tables, workspace, row_begin, row_end, ckpt,
                ckpt_first_row, stream)
+
+
+def _direct_call(name: str, shape, num_blocks: int, cache: torch.Tensor,
+                 block_tables: torch.Tensor, workspace: torch.Tensor,
+                 host: torch.Tensor, row_begin: int, row_end: int,
+                 ckpt_first_row: int, workgroups: int, stream):
+    R = block_tables.shape[0] if block_tables.dim() == 2 else -1
+    _check_tables(block_tables, R)
+    _check_cache(shape, num_blocks, cache, "cache")
+    if workspace.numel() * workspace.element_size() < \
+            lumen_kv_ckpt_plan_workspace_bytes(R):
+        raise ValueError("workspace too small for this many requests")
+    if host.is_cuda or not host.is_contiguous():
+        raise ValueError("host checkpoint must be a contiguous host tensor")
+    if host.numel() and not host.is_pinned():
+        raise ValueError("host checkpoint must be pinned (pin_memory=True)")
+    rb = _row_elems(shape) * _elem_bytes(shape)
+    if _nbytes(host) % rb:
+        raise ValueError("host checkpoint must hold whole rows")
+    rows = _nbytes(host) // rb
+    lay = layout(shape, num_blocks)
+    _check(getattr(load_library(), name)(
+        ctypes.byref(lay), _dev(cache, "cache"),
+        _dev(block_tables, "block_tables", torch.int32),
+        block_tables.shape[1], R, _dev(workspace, "workspace"),
+        int(row_begin), int(row_end),
+        ctypes.c_void_p(host.data_ptr() if host.numel() else None),
+        int(ckpt_first_row), rows, int(workgroups), _stream_handle(stream)),
+        name)
+
+
+def lumen_kv_ckpt_pack_to_host_direct(shape, num_blocks: int,
+                                      cache: torch.Tensor,
+                                      block_tables: torch.Tensor,
+                                      workspace: torch.Tensor,
+                                      host: torch.Tensor, row_begin: int = 0,
+                                      row_end: int = None,
+                                      ckpt_first_row: int = 0,
+                                      workgroups: int = 0,
+                                      stream: Optional[torch.cuda.Stream] = None):
+    """Pack the plan's packed rows [row_begin, row_end) straight into the
+    pinned host tensor `host`, a window holding checkpoint rows
+    [ckpt_first_row, ckpt_first_row + rows), on a grid of `workgroups`
+    workgroups (0: the library's default)."""
+    _direct_call("lumen_kv_ckpt_pack_to_host_direct", shape, num_blocks,
+                 cache, block_tables, workspace, host, row_begin,
+                 INT64_MAX if row_end is None else row_end, ckpt_first_row,
+                 workgroups, stream)
+
+
+def lumen_kv_ckpt_unpack_from_host_direct(shape, num_blocks: int,
+                                          cache: torch.Tensor,
+                                          block_tables: torch.Tensor,
+                                          workspace: torch.Tensor,
+                                          host: torch.Tensor,
+                                          row_begin: int = 0,
+                                          row_end: int = None,
+                                          ckpt_first_row: int = 0,
+                                          workgroups: int = 0,
+                                          stream: Optional[torch.cuda.Stream] = None):
+    """Unpack the plan's packed rows [row_begin, row_end) straight from the
+    pinned host tensor `host` (the window, as for the pack)."""
+    _direct_call("lumen_kv_ckpt_unpack_from_host_direct", shape, num_blocks,
+                 cache, block_tables, workspace, host, row_begin,
+                 INT64_MAX if row_end is None else row_end, ckpt_first_row,
+                 workgroups, stream)
 
 
 def _pipeline_args(shape, num_blocks, cache, block_tables, workspace,

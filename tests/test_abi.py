@@ -29,6 +29,8 @@ def test_exports_every_declared_entry_point(lib):
                           "lumen_kv_ckpt_unpack_rows",
                           "lumen_kv_ckpt_pack_to_host",
                           "lumen_kv_ckpt_unpack_from_host",
+                          "lumen_kv_ckpt_pack_to_host_direct",
+                          "lumen_kv_ckpt_unpack_from_host_direct",
                           "lumen_kv_draft_align"}
     for n in names:
         assert hasattr(lib, n), n
@@ -248,6 +250,32 @@ def test_pipeline_host_validation(lib):
         assert call(ws=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
         # nothing to move: no HIP call at all
         assert call(total=0, staging=None, host=None) == kv.LUMEN_OK
+        assert call(R=0) == kv.LUMEN_OK
+
+
+def test_direct_host_copy_validation(lib):
+    for name in ("lumen_kv_ckpt_pack_to_host_direct",
+                 "lumen_kv_ckpt_unpack_from_host_direct"):
+        f = getattr(lib, name)
+
+        def call(lay=None, R=2, ws=FAKE, lo=0, hi=10, first=0, rows=10,
+                 host=None, wg=0):
+            lay = _layout() if lay is None else lay
+            return f(ctypes.byref(lay), FAKE, FAKE, 4, R, ws, lo, hi, host,
+                     first, rows, wg, None)
+
+        assert call(wg=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(wg=4097) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(lo=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(lo=5, hi=4) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(first=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(rows=-1) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(ws=None) == kv.LUMEN_ERR_INVALID_ARG
+        assert call(lay=_layout(elem_bytes=3)) == kv.LUMEN_ERR_UNSUPPORTED
+        # a window of rows but no host memory: refused before any HIP call
+        assert call(host=None) == kv.LUMEN_ERR_INVALID_ARG
+        # an empty row range or no requests enqueues nothing
+        assert call(lo=7, hi=7) == kv.LUMEN_OK
         assert call(R=0) == kv.LUMEN_OK
 
 

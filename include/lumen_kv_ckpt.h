@@ -85,7 +85,7 @@ extern "C" {
 #define LUMEN_ERR_HIP (-4)         /* a HIP runtime call failed */
 #define LUMEN_ERR_RANGE (-5)       /* start < 0, end < start, or a page past bt_cols */
 #define LUMEN_ERR_BLOCK_ID (-6)    /* block table entry outside [0, num_blocks) */
-#define LUMEN_ERR_CAPACITY (-7)    /* checkpoint row outside [0, ckpt_rows) */
+#define LUMEN_ERR_CAPACITY (-7)    /* checkpoint row outside [0, ckpt_rows); host libraries: out of host memory */
 #define LUMEN_ERR_DUP_BLOCK (-8)   /* validate mode: a block named by two
                                       pages that an unpack would write */
 

@@ -58,14 +58,17 @@ void lumen_tag_store_destroy(lumen_tag_store *store);
  * page's payload has been received completely: that is what makes pages
  * atomic (a transfer cut short leaves its page invisible).  Pages may be
  * published in any order; publishing a page again replaces its tag.
- * INVALID_ARG for a null store, page < 0, or tag.end != (page + 1) *
- * block_size. */
+ * INVALID_ARG for a null store, page < 0, page > INT32_MAX, or tag.end !=
+ * (page + 1) * block_size.  CAPACITY if host memory for the page cannot be
+ * allocated; the store is then unchanged. */
 int lumen_tag_store_publish(lumen_tag_store *store, int64_t request,
                             int64_t page, lumen_page_tag tag);
 
 /* Computes the tags of pages [page_begin, page_end) from the token history
  * and publishes them (the receiver's call once those pages have arrived).
- * Same argument rules as lumen_page_tags. */
+ * Same argument rules as lumen_page_tags, and pages past INT32_MAX are
+ * INVALID_ARG; CAPACITY as for lumen_tag_store_publish (the pages before
+ * the failing one stay published). */
 int lumen_tag_store_publish_pages(lumen_tag_store *store, int64_t request,
                                   const int32_t *tokens, int64_t num_tokens,
                                   int64_t page_begin, int64_t page_end);

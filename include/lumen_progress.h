@@ -35,7 +35,9 @@ void lumen_progress_destroy(lumen_progress *p);
  * lengths[i]) and end[i] = lengths[i], then records end[i] as sent.  The
  * arrays are host memory, ready to be copied to the device for
  * lumen_kv_ckpt_plan.  INVALID_ARG for n < 0, a negative length, null
- * arrays with n > 0, or an id repeated in the batch (nothing changes then). */
+ * arrays with n > 0, or an id repeated in the batch; CAPACITY if host
+ * memory for new requests cannot be allocated.  Nothing changes on either
+ * error. */
 int lumen_progress_ranges(lumen_progress *p, const int64_t *ids,
                           const int32_t *lengths, int32_t n, int32_t *start,
                           int32_t *end);

@@ -59,8 +59,9 @@ int lumen_sched_set_worker(lumen_sched *s, int32_t worker,
 
 /* Eq. 1 for a new request served by `serving`: *holder receives the chosen
  * worker (the footprint is reserved there), or -1 if no worker can take
- * it.  Returns OK or INVALID_ARG (unknown worker, a request already
- * placed, a negative footprint, null holder). */
+ * it.  Returns OK, INVALID_ARG (unknown worker, a request already
+ * placed, a negative footprint, null holder), or CAPACITY if host memory
+ * for the request cannot be allocated (nothing changes then). */
 int lumen_sched_place(lumen_sched *s, int64_t request, int32_t serving,
                       int64_t reserved_bytes, int32_t *holder);
 
@@ -82,7 +83,8 @@ int64_t lumen_sched_reserved(lumen_sched *s, int32_t worker);
  * interrupted request, in increasing id, writes its id, the worker that
  * resumes it and whether it reuses its checkpoint (1) or is recomputed
  * (0); *num_out receives the count.  Returns INVALID_ARG if max_out is too
- * small (nothing changes then) or a worker index is bad. */
+ * small or a worker index is bad, CAPACITY if host memory for the
+ * decision cannot be allocated; nothing changes on either error. */
 int lumen_sched_recover(lumen_sched *s, const int32_t *failed,
                         int32_t num_failed, int64_t *out_request,
                         int32_t *out_worker, int8_t *out_reuse,

@@ -1508,7 +1508,9 @@ const char *lumen_kv_ckpt_strerror(int code) {
     case LUMEN_ERR_HIP: return "HIP runtime error";
     case LUMEN_ERR_RANGE: return "token range outside the request or its block table";
     case LUMEN_ERR_BLOCK_ID: return "block table entry outside the pool";
-    case LUMEN_ERR_CAPACITY: return "checkpoint row outside the checkpoint buffer";
+    case LUMEN_ERR_CAPACITY:
+      return "checkpoint row outside the checkpoint buffer, or host memory "
+             "exhausted";
     case LUMEN_ERR_DUP_BLOCK: return "block named by two pages of an unpack";
     default: return "unknown status";
   }

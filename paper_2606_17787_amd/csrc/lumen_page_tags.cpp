@@ -116,6 +116,10 @@ int check_pages(const int32_t *tokens, int64_t num_tokens, int32_t bs,
   return LUMEN_OK;
 }
 
+// Largest page index a store accepts (so (page + 1) * block_size and the
+// per-request page vector stay far from any overflow).
+constexpr int64_t kMaxPage = INT32_MAX;
+
 struct PageEntry {
   uint64_t hash = 0;
   int64_t end = 0;
@@ -157,15 +161,23 @@ void lumen_tag_store_destroy(lumen_tag_store *store) { delete store; }
 
 int lumen_tag_store_publish(lumen_tag_store *store, int64_t request,
                             int64_t page, lumen_page_tag tag) {
-  if (!store || page < 0 || tag.end != (page + 1) * store->block_size)
+  if (!store || page < 0 || page > kMaxPage ||
+      tag.end != (page + 1) * store->block_size)
     return LUMEN_ERR_INVALID_ARG;
   std::lock_guard<std::mutex> lock(store->mu);
-  std::vector<PageEntry> &v = store->pages[request];
-  if (v.size() <= size_t(page)) v.resize(size_t(page) + 1);
-  if (!v[page].visible) ++store->visible[request];
-  v[page].hash = tag.hash;
-  v[page].end = tag.end;
-  v[page].visible = true;
+  try {
+    // Everything that allocates happens before the page is changed, so a
+    // failed allocation leaves the store as it was.
+    std::vector<PageEntry> &v = store->pages[request];
+    if (v.size() <= size_t(page)) v.resize(size_t(page) + 1);
+    int64_t &count = store->visible[request];
+    if (!v[page].visible) ++count;
+    v[page].hash = tag.hash;
+    v[page].end = tag.end;
+    v[page].visible = true;
+  } catch (const std::bad_alloc &) {
+    return LUMEN_ERR_CAPACITY;
+  }
   return LUMEN_OK;
 }
 

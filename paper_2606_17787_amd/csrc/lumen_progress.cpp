@@ -28,17 +28,24 @@ int lumen_progress_ranges(lumen_progress *p, const int64_t *ids,
   if (!p || n < 0) return LUMEN_ERR_INVALID_ARG;
   if (n > 0 && (!ids || !lengths || !start || !end))
     return LUMEN_ERR_INVALID_ARG;
-  std::unordered_set<int64_t> seen;
-  for (int32_t i = 0; i < n; ++i) {
-    if (lengths[i] < 0 || !seen.insert(ids[i]).second)
-      return LUMEN_ERR_INVALID_ARG;
+  try {
+    std::unordered_set<int64_t> seen;
+    for (int32_t i = 0; i < n; ++i) {
+      if (lengths[i] < 0 || !seen.insert(ids[i]).second)
+        return LUMEN_ERR_INVALID_ARG;
+    }
+    // Allocation first: a request not seen before gets an entry of 0 sent
+    // tokens, which is what an absent entry means, so a failure here
+    // changes nothing a caller can observe.
+    for (int32_t i = 0; i < n; ++i) p->sent.emplace(ids[i], 0);
+  } catch (const std::bad_alloc &) {
+    return LUMEN_ERR_CAPACITY;
   }
   for (int32_t i = 0; i < n; ++i) {
-    auto it = p->sent.find(ids[i]);
-    const int32_t done = it == p->sent.end() ? 0 : it->second;
+    int32_t &done = p->sent.find(ids[i])->second;
     start[i] = done < lengths[i] ? done : lengths[i];
     end[i] = lengths[i];
-    p->sent[ids[i]] = lengths[i];
+    done = lengths[i];
   }
   return LUMEN_OK;
 }

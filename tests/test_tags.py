@@ -198,6 +198,13 @@ def test_native_argument_errors():
         st.publish(1, -1, 123, 0)
     with pytest.raises(kv.LumenError):
         st.publish_pages(1, tok, 0, 3)  # page 2 is not complete
+    # page indices past INT32_MAX are refused before (page + 1) * block_size
+    # is formed or any page vector grows
+    for page in ((1 << 31), (1 << 62), (1 << 63) - 1):
+        with pytest.raises(kv.LumenError) as e:
+            st.publish(1, page, 123, ((page + 1) * 4) % (1 << 63))
+        assert e.value.code == kv.LUMEN_ERR_INVALID_ARG
+    assert st.pages(1) == 0
     with pytest.raises(kv.LumenError):
         T.TagStore(0)
 

@@ -139,6 +139,10 @@ def _stream_handle(stream: Optional[torch.cuda.Stream]):
 def _dev(t: torch.Tensor, what: str, dtype=None) -> ctypes.c_void_p:
     if not t.is_cuda:
         raise ValueError(f"{what} must be a device tensor")
+    if t.device.index != torch.cuda.current_device():
+        # the library launches on the current device
+        raise ValueError(f"{what} is on {t.device}, the current device is "
+                         f"cuda:{torch.cuda.current_device()}")
     if not t.is_contiguous():
         raise ValueError(f"{what} must be contiguous")
     if dtype is not None and t.dtype != dtype:

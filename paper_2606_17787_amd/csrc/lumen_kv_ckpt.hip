@@ -426,9 +426,11 @@ __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_
     int64_t row_end2 = row_end, t2 = t + 1, crow2 = crow + 1;
     if (more && row + 1 == row_end) {
       // Next request with rows; one exists because row + 1 < total_rows.
+      // The bound keeps the walk inside the plan even if a caller has
+      // overwritten the workspace (a valid plan never reaches it).
       do {
         ++r2;
-      } while (prefix[r2 + 1] == row + 1);
+      } while (r2 + 1 < g.num_reqs && prefix[r2 + 1] == row + 1);
       row_end2 = prefix[r2 + 1];
       t2 = start[r2];
       crow2 = first_row[r2] - g.win_first;

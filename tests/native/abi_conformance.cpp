@@ -1,0 +1,214 @@
+// C ABI conformance: a plain HIP host program (no Python, no torch) that
+// drives liblumen_kv_ckpt through include/lumen_kv_ckpt.h with its own
+// hipMalloc'd buffers and stream, and checks every result against the C
+// oracle (oracle/lumen_oracle.h) on the same inputs, byte for byte.
+//
+// Cases: a token-major cache of 2-byte elements and a head-major cache of
+// 4-byte elements; packed and per-request row plans; restore into a second
+// pool under another block table; a poisoned block-table entry; the direct
+// copy into pinned host memory.  Built by tests/native/build.py, run by
+// tests/test_gpu_abi_c.py.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "lumen_kv_ckpt.h"
+#include "../../oracle/lumen_oracle.h"
+
+#define HIP_OK(x)                                                       \
+  do {                                                                  \
+    hipError_t e_ = (x);                                                \
+    if (e_ != hipSuccess) {                                             \
+      fprintf(stderr, "%s:%d %s: %s\n", __FILE__, __LINE__, #x,         \
+              hipGetErrorString(e_));                                   \
+      exit(2);                                                          \
+    }                                                                   \
+  } while (0)
+#define CHECK(c)                                                        \
+  do {                                                                  \
+    if (!(c)) {                                                         \
+      fprintf(stderr, "check failed at line %d: %s\n", __LINE__, #c);   \
+      exit(1);                                                          \
+    }                                                                   \
+  } while (0)
+
+// Seeded test inputs (splitmix64); holds none of the method's arithmetic.
+struct Rng {
+  uint64_t s;
+  uint64_t next() {
+    uint64_t z = (s += 0x9e3779b97f4a7c15ull);
+    z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+    z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+    return z ^ (z >> 31);
+  }
+  int64_t below(int64_t n) { return int64_t(next() % uint64_t(n)); }
+};
+
+template <class T>
+T *dev_copy(const std::vector<T> &h) {
+  T *d = nullptr;
+  HIP_OK(hipMalloc(&d, std::max<size_t>(h.size(), 1) * sizeof(T)));
+  if (!h.empty())
+    HIP_OK(hipMemcpy(d, h.data(), h.size() * sizeof(T), hipMemcpyHostToDevice));
+  return d;
+}
+
+template <class T>
+std::vector<T> host_copy(const T *d, size_t n) {
+  std::vector<T> h(n);
+  if (n) HIP_OK(hipMemcpy(h.data(), d, n * sizeof(T), hipMemcpyDeviceToHost));
+  return h;
+}
+
+struct Case {
+  int32_t L, H, D, bs, NB, R, cols, elem, head_major;
+};
+
+static void run_case(const Case &c, uint64_t seed, hipStream_t stream) {
+  Rng rng{seed};
+  lumen_kv_layout lay;
+  lay.num_layers = c.L;
+  lay.num_kv_heads = c.H;
+  lay.head_dim = c.D;
+  lay.block_size = c.bs;
+  lay.num_blocks = c.NB;
+  lay.elem_bytes = c.elem;
+  lay.cache_order = c.head_major ? LUMEN_CACHE_HND : LUMEN_CACHE_NHD;
+  oracle_cache_shape osh;
+  osh.num_layers = c.L;
+  osh.num_kv_heads = c.H;
+  osh.head_dim = c.D;
+  osh.block_size = c.bs;
+  osh.num_blocks = c.NB;
+  osh.head_major = c.head_major;
+  osh.elem_bytes = c.elem;
+
+  const size_t pool_bytes =
+      size_t(c.L) * 2 * c.NB * c.bs * c.H * c.D * size_t(c.elem);
+  const size_t row_bytes = size_t(c.L) * 2 * c.H * c.D * c.elem;
+  std::vector<uint8_t> src(pool_bytes), dst(pool_bytes);
+  for (auto &x : src) x = uint8_t(rng.next());
+  for (auto &x : dst) x = uint8_t(rng.next());
+
+  // Two block tables naming distinct blocks, and token ranges inside them
+  // (one empty range, one starting mid-page).
+  CHECK(c.R * c.cols <= c.NB);
+  std::vector<int32_t> perm(c.NB), perm2(c.NB);
+  for (int32_t i = 0; i < c.NB; ++i) perm[i] = perm2[i] = i;
+  for (int32_t i = c.NB - 1; i > 0; --i) {
+    std::swap(perm[i], perm[rng.below(i + 1)]);
+    std::swap(perm2[i], perm2[rng.below(i + 1)]);
+  }
+  std::vector<int32_t> bt(perm.begin(), perm.begin() + c.R * c.cols);
+  std::vector<int32_t> bt2(perm2.begin(), perm2.begin() + c.R * c.cols);
+  std::vector<int32_t> s(c.R), e(c.R);
+  const int32_t cap = c.cols * c.bs;
+  for (int32_t r = 0; r < c.R; ++r) {
+    s[r] = int32_t(rng.below(cap));
+    e[r] = s[r] + int32_t(rng.below(cap - s[r] + 1));
+  }
+  e[0] = s[0];  // an empty range
+  int64_t total = 0;
+  for (int32_t r = 0; r < c.R; ++r) total += e[r] - s[r];
+  CHECK(total > 0);
+
+  // Oracle on the host.
+  std::vector<uint8_t> want(size_t(total) * row_bytes);
+  CHECK(oracle_pack(&osh, src.data(), bt.data(), c.cols, s.data(), e.data(),
+                    c.R, 0, nullptr, want.data(), total) == ORACLE_OK);
+  std::vector<uint8_t> want_dst = dst;
+  CHECK(oracle_unpack(&osh, want_dst.data(), bt2.data(), c.cols, s.data(),
+                      e.data(), c.R, 0, nullptr, want.data(),
+                      total) == ORACLE_OK);
+
+  // The library on the device.
+  uint8_t *d_src = dev_copy(src), *d_dst = dev_copy(dst);
+  int32_t *d_bt = dev_copy(bt), *d_bt2 = dev_copy(bt2);
+  int32_t *d_s = dev_copy(s), *d_e = dev_copy(e);
+  void *ws = nullptr;
+  HIP_OK(hipMalloc(&ws, lumen_kv_ckpt_plan_workspace_bytes(c.R)));
+  uint8_t *d_ck = nullptr;
+  HIP_OK(hipMalloc(&d_ck, size_t(total) * row_bytes));
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_pack(&lay, d_src, d_bt, c.cols, c.R, ws, d_ck, total,
+                           stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_status(ws, stream) == LUMEN_OK);
+  CHECK(host_copy(d_ck, want.size()) == want);
+  CHECK(lumen_kv_ckpt_unpack(&lay, d_dst, d_bt2, c.cols, c.R, ws, d_ck, total,
+                             stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_status(ws, stream) == LUMEN_OK);
+  CHECK(host_copy(d_dst, pool_bytes) == want_dst);
+
+  // Per-request row mode: request r's token t at row base[r] + t.
+  std::vector<int64_t> base(c.R);
+  int64_t next = 3;
+  for (int32_t r = 0; r < c.R; ++r) {
+    base[r] = next - s[r];
+    next += (e[r] - s[r]) + 1;  // a gap row after each request
+  }
+  const int64_t rows2 = next;
+  std::vector<uint8_t> want2(size_t(rows2) * row_bytes, 0xA5);
+  CHECK(oracle_pack(&osh, src.data(), bt.data(), c.cols, s.data(), e.data(),
+                    c.R, 0, base.data(), want2.data(), rows2) == ORACLE_OK);
+  int64_t *d_base = dev_copy(base);
+  uint8_t *d_ck2 = dev_copy(std::vector<uint8_t>(want2.size(), 0xA5));
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, d_base, ws, stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_pack(&lay, d_src, d_bt, c.cols, c.R, ws, d_ck2, rows2,
+                           stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_status(ws, stream) == LUMEN_OK);
+  CHECK(host_copy(d_ck2, want2.size()) == want2);
+
+  // A block-table entry outside the pool: the oracle's status.
+  std::vector<int32_t> bad = bt;
+  int32_t rb = 1;
+  while (e[rb] == s[rb]) ++rb;  // a request with tokens (rb < R: total > 0)
+  bad[size_t(rb) * c.cols + s[rb] / c.bs] = c.NB + 7;
+  const int want_st = oracle_pack(&osh, src.data(), bad.data(), c.cols,
+                                  s.data(), e.data(), c.R, 0, nullptr,
+                                  want.data(), total);
+  CHECK(want_st == ORACLE_ERR_BLOCK_ID);
+  int32_t *d_bad = dev_copy(bad);
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_pack(&lay, d_src, d_bad, c.cols, c.R, ws, d_ck, total,
+                           stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_status(ws, stream) == want_st);
+
+  // The direct copy into pinned host memory.
+  uint8_t *h_ck = nullptr;
+  HIP_OK(hipHostMalloc((void **)&h_ck, size_t(total) * row_bytes,
+                       hipHostMallocDefault));
+  memset(h_ck, 0, size_t(total) * row_bytes);
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_pack_to_host_direct(&lay, d_src, d_bt, c.cols, c.R, ws,
+                                          0, INT64_MAX, h_ck, 0, total, 0,
+                                          stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_status(ws, stream) == LUMEN_OK);
+  CHECK(memcmp(h_ck, want.data(), want.size()) == 0);
+
+  HIP_OK(hipHostFree(h_ck));
+  for (void *p : {(void *)d_src, (void *)d_dst, (void *)d_bt, (void *)d_bt2,
+                  (void *)d_s, (void *)d_e, ws, (void *)d_ck, (void *)d_base,
+                  (void *)d_ck2, (void *)d_bad})
+    HIP_OK(hipFree(p));
+}
+
+int main() {
+  hipStream_t stream = nullptr;
+  HIP_OK(hipStreamCreate(&stream));  // default priority
+  const Case cases[] = {
+      {3, 2, 64, 16, 64, 5, 4, 2, 0},  // token-major, 2-byte elements
+      {2, 3, 8, 5, 40, 4, 6, 4, 1},    // head-major, 4-byte elements
+  };
+  uint64_t seed = 20261202;
+  for (const Case &c : cases)
+    for (int rep = 0; rep < 3; ++rep) run_case(c, seed++, stream);
+  HIP_OK(hipStreamDestroy(stream));
+  printf("abi conformance ok: %zu layouts x 3 seeds\n",
+         sizeof(cases) / sizeof(cases[0]));
+  return 0;
+}

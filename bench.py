@@ -168,7 +168,74 @@ def incremental_leg(torch, kv, w, steps, warmup, seed):
     roundtrip = bool(torch.equal(back.view(torch.int16),
                                  region.view(torch.int16)))
     assert kv.lumen_kv_ckpt_status(ws_b) == 0
-    del src, dst, arena, back
+
+    # The per-request row mode: one checkpoint per request (Sec. 4.2), the
+    # increments of request r appending to its own region of the same
+    # arena, so a step's rows land in up to R places instead of one run.
+    inc = w.ends[-1].astype(np.int64) - w.starts[0].astype(np.int64)
+    assert int(inc.sum()) == int(row_off[-1])
+    region0 = np.concatenate([[0], np.cumsum(inc)[:-1]])
+    rrb_h = region0 - w.starts[0].astype(np.int64)  # row of token t: rrb + t
+    rrb = torch.from_numpy(rrb_h).to(dev)
+    for k in range(S):
+        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
+        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
+    assert kv.lumen_kv_ckpt_status(ws_a) == 0
+    pr_steps = max(steps // 2, EVENT_EVERY)
+    pr_ev = {i: [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+             for i in range(0, pr_steps, EVENT_EVERY)}
+
+    def step_pr(i, events=None):
+        k = i % S
+        k2 = (k + S // 2) % S
+        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
+        if events: events[0].record()
+        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
+        if events: events[1].record()
+        kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, 0, rrb)
+        if events: events[2].record()
+        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt_dst, ws_b,
+                                arena)
+        if events: events[3].record()
+        return k, k2
+
+    for i in range(warmup):
+        step_pr(i)
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    pr_done = [step_pr(warmup + i, pr_ev.get(i)) for i in range(pr_steps)]
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+    assert min(kv.lumen_kv_ckpt_status(ws_a),
+               kv.lumen_kv_ckpt_status(ws_b)) == 0
+    pr_s = sorted(pr_ev)
+    pr_pack_b = sum(2.0 * rows[pr_done[i][0]] * rb for i in pr_s)
+    pr_unpack_b = sum(2.0 * rows[pr_done[i][1]] * rb for i in pr_s)
+    pr_pack_ms = sum(pr_ev[i][0].elapsed_time(pr_ev[i][1]) for i in pr_s)
+    pr_unpack_ms = sum(pr_ev[i][2].elapsed_time(pr_ev[i][3]) for i in pr_s)
+    pr_step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in pr_done)
+    # self-check: one step's rows, gathered from the request regions, equal
+    # the same step packed contiguously
+    k = pr_done[-1][0]
+    kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0)
+    back = torch.empty(int(rows[k]) * row_elems, dtype=torch.bfloat16,
+                       device=dev)
+    kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, back)
+    idx = np.concatenate([np.arange(rrb_h[r] + w.starts[k][r],
+                                    rrb_h[r] + w.ends[k][r])
+                          for r in range(w.num_reqs)]).astype(np.int64)
+    gathered = arena.view(-1, row_elems).index_select(
+        0, torch.from_numpy(idx).to(dev))
+    pr_ok = bool(torch.equal(gathered.view(torch.int16).reshape(-1),
+                             back.view(torch.int16)))
+    assert kv.lumen_kv_ckpt_status(ws_a) == 0
+    per_request_mode = dict(
+        steps=pr_steps, ms_per_step=(t3 - t2) * 1e3 / pr_steps,
+        step_GBps=gb(pr_step_b) / (t3 - t2),
+        pack_GBps=gb(pr_pack_b) / (pr_pack_ms / 1e3),
+        unpack_GBps=gb(pr_unpack_b) / (pr_unpack_ms / 1e3),
+        check_ok=pr_ok)
+    del src, dst, arena, back, gathered
     torch.cuda.empty_cache()
 
     pack_GBps = gb(pack_b.sum()) / (pack_ms.sum() / 1e3)
@@ -192,6 +259,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed):
         unpack_bytes_mean=float(unpack_b.mean()),
         tokens_per_step_mean=float(rows.mean()),
         roundtrip_ok=roundtrip,
+        per_request_mode=per_request_mode,
     )
 
 
@@ -1000,6 +1068,8 @@ def rounded(d):
             return round(v, 4)
         if isinstance(v, list):
             return [r(x) for x in v]
+        if isinstance(v, dict):
+            return {k: r(x) for k, x in v.items()}
         return v
     return {k: r(v) for k, v in d.items()}
 
@@ -1048,6 +1118,7 @@ def main():
         "pack_us_mean": round(dec["pack_us_mean"], 2),
         "unpack_us_mean": round(dec["unpack_us_mean"], 2),
         "roundtrip_ok": dec["roundtrip_ok"],
+        "per_request_mode": rounded(dec["per_request_mode"]),
         "roofline": {"bound": "hbm",
                      "kernel": "copy_rows_kernel<%s, false> (%s)" % (
                          "true" if dominant == "pack" else "false", dominant),

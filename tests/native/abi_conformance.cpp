@@ -6,8 +6,9 @@
 // Cases: a token-major cache of 2-byte elements and a head-major cache of
 // 4-byte elements; packed and per-request row plans; restore into a second
 // pool under another block table; a poisoned block-table entry; the direct
-// copy into pinned host memory.  Built by tests/native/build.py, run by
-// tests/test_gpu_abi_c.py.
+// copy into pinned host memory; both staging pipelines on streams of the
+// program's own; validate mode with and without a duplicate target.  Built
+// by tests/native/build.py, run by tests/test_gpu_abi_c.py.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -190,6 +191,71 @@ static void run_case(const Case &c, uint64_t seed, hipStream_t stream) {
   CHECK(lumen_kv_ckpt_status(ws, stream) == LUMEN_OK);
   CHECK(memcmp(h_ck, want.data(), want.size()) == 0);
 
+  // The staging pipelines: to pinned host memory through a 2-slot ring,
+  // and back into a third pool, on streams of the program's own.
+  hipStream_t ps = nullptr, cs = nullptr, us = nullptr;
+  HIP_OK(hipStreamCreate(&ps));
+  HIP_OK(hipStreamCreate(&cs));
+  HIP_OK(hipStreamCreate(&us));
+  const int64_t slot_rows = 3;
+  uint8_t *d_ring = nullptr;
+  HIP_OK(hipMalloc(&d_ring, 2 * slot_rows * row_bytes));
+  memset(h_ck, 0, size_t(total) * row_bytes);
+  HIP_OK(hipStreamSynchronize(stream));
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, ps) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_pack_to_host(&lay, d_src, d_bt, c.cols, c.R, ws, total,
+                                   d_ring, slot_rows, 2, h_ck, ps,
+                                   cs) == LUMEN_OK);
+  HIP_OK(hipStreamSynchronize(cs));
+  CHECK(lumen_kv_ckpt_status(ws, ps) == LUMEN_OK);
+  CHECK(memcmp(h_ck, want.data(), want.size()) == 0);
+  uint8_t *d_dst3 = dev_copy(dst);
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, us) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_unpack_from_host(&lay, d_dst3, d_bt2, c.cols, c.R, ws,
+                                       total, h_ck, d_ring, slot_rows, 2, cs,
+                                       us) == LUMEN_OK);
+  HIP_OK(hipStreamSynchronize(us));
+  CHECK(lumen_kv_ckpt_status(ws, us) == LUMEN_OK);
+  CHECK(host_copy(d_dst3, pool_bytes) == want_dst);
+
+  // Validate mode: the restore table passes; a second page naming an
+  // already written block is DUP_BLOCK, as the oracle says.
+  const size_t mb = lumen_kv_ckpt_marks_bytes(c.NB);
+  void *d_marks = nullptr;
+  HIP_OK(hipMalloc(&d_marks, mb));
+  CHECK(oracle_validate_targets(&osh, bt2.data(), c.cols, s.data(), e.data(),
+                                c.R) == ORACLE_OK);
+  CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_validate_targets(&lay, d_bt2, c.cols, c.R, ws, d_marks,
+                                       mb, stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_status(ws, stream) == LUMEN_OK);
+  std::vector<int32_t> dup = bt2;
+  int32_t ra = -1, rb2 = -1;  // two requests whose ranges write pages
+  for (int32_t r = 0; r < c.R; ++r)
+    if (e[r] > s[r]) {
+      if (ra < 0) ra = r; else if (rb2 < 0) rb2 = r;
+    }
+  if (ra >= 0 && rb2 >= 0) {
+    dup[size_t(rb2) * c.cols + s[rb2] / c.bs] =
+        dup[size_t(ra) * c.cols + s[ra] / c.bs];
+    const int want_v = oracle_validate_targets(&osh, dup.data(), c.cols,
+                                               s.data(), e.data(), c.R);
+    CHECK(want_v == ORACLE_ERR_DUP_BLOCK);
+    int32_t *d_dup = dev_copy(dup);
+    CHECK(lumen_kv_ckpt_plan(d_s, d_e, c.R, 0, nullptr, ws, stream) ==
+          LUMEN_OK);
+    CHECK(lumen_kv_ckpt_validate_targets(&lay, d_dup, c.cols, c.R, ws,
+                                         d_marks, mb, stream) == LUMEN_OK);
+    CHECK(lumen_kv_ckpt_status(ws, stream) == want_v);
+    HIP_OK(hipFree(d_dup));
+  }
+  CHECK(strcmp(lumen_kv_ckpt_strerror(LUMEN_ERR_DUP_BLOCK), "unknown status"));
+  CHECK(!strcmp(lumen_kv_ckpt_strerror(12345), "unknown status"));
+
+  HIP_OK(hipFree(d_marks));
+  HIP_OK(hipFree(d_dst3));
+  HIP_OK(hipFree(d_ring));
+  for (hipStream_t q : {ps, cs, us}) HIP_OK(hipStreamDestroy(q));
   HIP_OK(hipHostFree(h_ck));
   for (void *p : {(void *)d_src, (void *)d_dst, (void *)d_bt, (void *)d_bt2,
                   (void *)d_s, (void *)d_e, ws, (void *)d_ck, (void *)d_base,

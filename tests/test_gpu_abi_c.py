@@ -1,8 +1,8 @@
 """The C ABI used from a plain HIP host program, without Python or torch:
-tests/native/abi_conformance allocates its own buffers and stream, runs
-plan, pack, unpack, status and the direct host copy through
-include/lumen_kv_ckpt.h, and compares every result with the C oracle byte
-for byte (two layouts, three seeds each).  __graft_entry__.build() builds
+tests/native/abi_conformance allocates its own buffers and streams, runs
+plan, pack, unpack, status, the direct host copy, both staging pipelines and
+validate mode through include/lumen_kv_ckpt.h, and compares every result
+with the C oracle byte for byte (two layouts, three seeds each).  __graft_entry__.build() builds
 it."""
 import os
 import subprocess

@@ -1,0 +1,134 @@
+"""Seeded random configurations against the oracle: each draws a cache shape
+(layers, heads, head_dim, block size, element width, NHD or HND), a request
+count, block tables, token ranges (empty ones included), the plan mode
+(packed from a row base, or per-request rows) and a grid size, then checks
+pack, unpack, windowed packs and the direct host copy element by element.
+One configuration in eight plants an error (a page past the table, or a
+block id outside the pool); then only the status is compared, since the GPU
+still copies the rows that are fine while the oracle writes nothing."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_17787_amd.kvckpt as kv
+from paper_2606_17787_amd import workloads as W
+from paper_2606_17787_amd.workloads import CacheShape, HND, NHD
+
+from gpu_util import SENTINEL, d2h_words, dev, h2d
+
+pytestmark = pytest.mark.gpu
+
+WORD = {1: np.uint8, 2: np.uint16, 4: np.uint32}
+
+
+def draw(seed):
+    rng = np.random.default_rng(5000 + seed)
+    elem = int(rng.choice([1, 2, 4]))
+    D = (16 // elem) * int(rng.integers(1, 9))  # D*elem a multiple of 16
+    shape = CacheShape(int(rng.integers(1, 6)), int(rng.integers(1, 7)), D,
+                       int(rng.integers(1, 41)),
+                       HND if rng.random() < 0.5 else NHD, elem)
+    R = int(rng.integers(1, 41))
+    cols = int(rng.integers(1, 9))
+    nb = R * cols + int(rng.integers(0, 9))
+    perm = rng.permutation(nb).astype(np.int32)
+    bt = perm[:R * cols].reshape(R, cols).copy()
+    bt2 = rng.permutation(nb).astype(np.int32)[:R * cols].reshape(R, cols)
+    cap = cols * shape.block_size
+    s = rng.integers(0, cap + 1, R).astype(np.int32)
+    e = np.minimum(s + rng.integers(0, cap + 1, R), cap).astype(np.int32)
+    empty = rng.random(R) < 0.2
+    e[empty] = s[empty]
+    error = None
+    if rng.random() < 0.125 and (e > s).any():
+        r = int(np.flatnonzero(e > s)[0])
+        if rng.random() < 0.5:
+            bt[r, s[r] // shape.block_size] = nb + 3  # BLOCK_ID
+            error = "block"
+        else:
+            e[r] = cap + int(rng.integers(1, 5))      # RANGE: past the table
+            error = "range"
+    per_request = rng.random() < 0.3
+    row_base = int(rng.integers(0, 5))
+    waves = int(rng.choice([0, 1, 7, 64]))
+    src = W.random_words(rng, shape.pool_elems(nb), elem)
+    dst = W.random_words(rng, shape.pool_elems(nb), elem)
+    return (rng, shape, R, nb, bt, bt2, s, e, error, per_request, row_base,
+            waves, src, dst)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_configuration_matches_oracle(seed):
+    (rng, shape, R, nb, bt, bt2, s, e, error, per_request, row_base, waves,
+     src, dst) = draw(seed)
+    eb, re_ = shape.elem_bytes, shape.token_row_elems
+    n = np.maximum(e.astype(np.int64) - s, 0)
+    if per_request:
+        base = np.concatenate([[0], np.cumsum(n + 1)[:-1]]) - s + 2
+        ck_rows = int((n + 1).sum()) + 2
+        kw = dict(req_row_base=base)
+    else:
+        base = None
+        ck_rows = int(n.sum()) + row_base
+        kw = dict(row_base=row_base)
+    want_ck = np.full((max(ck_rows, 0), re_), SENTINEL, WORD[eb])
+    st_o, want_ck = oracle.pack(shape, nb, src, bt, s, e, ckpt=want_ck, **kw)
+    want_dst = dst.copy()
+    if st_o == oracle.OK:
+        assert oracle.unpack(shape, nb, want_dst, bt2, s, e, want_ck,
+                             **kw) == oracle.OK
+    if error:
+        assert st_o != oracle.OK
+
+    d_src, d_bt, d_bt2 = h2d(src), h2d(bt), h2d(bt2)
+    d_s, d_e = h2d(s), h2d(e)
+    d_base = None if base is None else h2d(base.astype(np.int64))
+    ws = kv.new_workspace(R, dev())
+    ck = h2d(np.full(max(ck_rows, 1) * re_, SENTINEL, WORD[eb]))
+    ck_view = ck[:ck_rows * re_]
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, 0 if per_request else row_base,
+                          d_base)
+    kv.lumen_kv_ckpt_pack(shape, nb, d_src, d_bt, ws, ck_view)
+    st_g = kv.lumen_kv_ckpt_status(ws)
+    assert st_g == st_o, (seed, st_g, st_o)
+    if st_o != oracle.OK:
+        return
+    assert np.array_equal(d2h_words(ck_view, eb).reshape(-1, re_), want_ck)
+
+    # restore into another pool under the second table
+    d_dst = h2d(dst)
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, 0 if per_request else row_base,
+                          d_base)
+    kv.lumen_kv_ckpt_unpack(shape, nb, d_dst, d_bt2, ws, ck_view)
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    assert np.array_equal(d2h_words(d_dst, eb), want_dst)
+
+    # the direct copy into pinned host memory, on a drawn grid size
+    host = torch.empty((ck_rows * re_ * eb,), dtype=torch.uint8,
+                       pin_memory=True)
+    host.numpy().view(WORD[eb])[:] = SENTINEL  # the oracle's untouched rows
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, 0 if per_request else row_base,
+                          d_base)
+    kv.lumen_kv_ckpt_pack_to_host_direct(shape, nb, d_src, d_bt, ws, host,
+                                         workgroups=waves)
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    got = host.numpy().view(WORD[eb]).reshape(-1, re_)
+    assert np.array_equal(got, want_ck)
+
+    # windowed packs of random chunk sizes (packed mode: a chunk of packed
+    # rows [lo, hi) is the window of checkpoint rows row_base + [lo, hi))
+    total = int(n.sum())
+    if not per_request and total:
+        k = int(rng.integers(1, total + 1))
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws, row_base)
+        parts = []
+        for lo in range(0, total, k):
+            hi = min(lo + k, total)
+            win = torch.zeros((hi - lo) * re_, dtype=ck.dtype, device=dev())
+            kv.lumen_kv_ckpt_pack_rows(shape, nb, d_src, d_bt, ws, lo, hi,
+                                       win, ckpt_first_row=row_base + lo)
+            parts.append(win)
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+        got = np.concatenate([d2h_words(p, eb) for p in parts])
+        assert np.array_equal(got.reshape(-1, re_), want_ck[row_base:])

@@ -134,7 +134,14 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
  * checked in this order: page t/block_size < bt_cols (RANGE); block id in
  * [0, num_blocks) (BLOCK_ID); row in [0, ckpt_rows) (CAPACITY).  num_reqs
  * must equal the plan's.  d_cache and d_ckpt 16-byte aligned; a buffer may
- * be NULL only if it is empty (num_blocks, ckpt_rows or bt_cols is 0). */
+ * be NULL only if it is empty (num_blocks, ckpt_rows or bt_cols is 0).
+ *
+ * Grid size.  The plan's row count lives in device memory, so the launch is
+ * sized without it: 384 wavefronts per CU (LUMEN_KV_CKPT_WAVES_PER_CU in the
+ * environment overrides this), but never more than one per (row, layer)
+ * unit that ckpt_rows (or the row range of the _rows calls) could hold.  A
+ * checkpoint buffer or window sized to the plan's rows keeps small steps
+ * free of idle wavefronts. */
 int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
                        const int32_t *d_block_tables, int32_t bt_cols,
                        int32_t num_reqs, void *d_workspace, void *d_ckpt,

@@ -141,7 +141,13 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
  * environment overrides this), but never more than one per (row, layer)
  * unit that ckpt_rows (or the row range of the _rows calls) could hold.  A
  * checkpoint buffer or window sized to the plan's rows keeps small steps
- * free of idle wavefronts. */
+ * free of idle wavefronts.
+ *
+ * Walk.  A pack of a token-major cache whose token runs (H*D*elem_bytes
+ * bytes per layer and K/V) are at most 512 bytes is done page by page: whole
+ * page runs are read, and each token's piece is written to its row.  The
+ * environment variable LUMEN_KV_CKPT_PAGE_MAJOR=0 or 1 forces this off or
+ * on.  The result and the status are the same either way. */
 int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
                        const int32_t *d_block_tables, int32_t bt_cols,
                        int32_t num_reqs, void *d_workspace, void *d_ckpt,

@@ -15,6 +15,8 @@ Infinity Cache.  Inputs (pools, block tables, ranges) are resident in HBM
 before timing; the device error word is checked after the timed loop.
 
 Further legs (reported beside the headline, not part of its value):
+  * tiny            the 8-request, 1.77 MB full pack and restore: launch
+                    latency, back-to-back rate and host enqueue cost
   * qwen-gqa-hnd    the same decode loop on the head-major Qwen-style cache
   * qwen-gqa-nhd-twin  the same requests and tables over a token-major cache
                     (what the head-major transpose costs)
@@ -52,8 +54,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
-ALL_LEGS = ("decode", "qwen", "restore", "tp8", "stage", "tags", "sched",
-            "draft", "cpu")
+ALL_LEGS = ("decode", "tiny", "qwen", "restore", "tp8", "stage", "tags",
+            "sched", "draft", "cpu")
 EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step
 
 
@@ -923,6 +925,87 @@ def draft_leg(torch, kv, reps=50):
             "freed_blocks": int(cnt.item()), "check_ok": ok}
 
 
+def tiny_leg(torch, kv, W, reps=200):
+    """The tiny full-pack workload (2 layers, 2 KV heads, head_dim 64,
+    block 16; 8 requests, 1,729 tokens, 1.77 MB each way) is launch-bound,
+    so it reports latency: device us of plan + pack and of plan + unpack
+    from HIP events around each pair with the stream drained in between,
+    the same pairs back to back, and the host cost of enqueueing one call
+    through the binding.  Self-check: the restored tokens, packed again
+    from the destination pool, equal the checkpoint."""
+    dev = torch.device("cuda:0")
+    w = W.c1_tiny()
+    sh = w.shape
+    rows = w.step_tokens(0)
+    src = torch.from_numpy(W.random_bits(np.random.default_rng(1),
+                                         sh.pool_elems(w.num_blocks))
+                           .view(np.int16)).to(dev)
+    dst = torch.zeros(sh.pool_elems(w.dst_num_blocks), dtype=torch.int16,
+                      device=dev)
+    ck = torch.empty(rows * sh.token_row_elems, dtype=torch.int16, device=dev)
+    back = torch.empty_like(ck)
+    bt = torch.from_numpy(w.block_tables).to(dev)
+    bt2 = torch.from_numpy(w.dst_block_tables).to(dev)
+    s = torch.from_numpy(w.starts[0]).to(dev)
+    e = torch.from_numpy(w.ends[0]).to(dev)
+    ws = kv.new_workspace(w.num_reqs, dev)
+
+    def pack():
+        kv.lumen_kv_ckpt_plan(s, e, ws)
+        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws, ck)
+
+    def unpack():
+        kv.lumen_kv_ckpt_plan(s, e, ws)
+        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt2, ws, ck)
+
+    def pair_us(fn):
+        out = []
+        for i in range(reps + 20):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            b.synchronize()
+            if i >= 20:
+                out.append(a.elapsed_time(b) * 1e3)
+        return out
+
+    pk, up = pair_us(pack), pair_us(unpack)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        pack()
+        unpack()
+    b.record()
+    b.synchronize()
+    rt_us = a.elapsed_time(b) * 1e3 / reps
+    # host cost of one enqueue (binding + C ABI), the stream left to run
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws, ck)
+    host_us = (time.perf_counter() - t0) * 1e6 / reps
+    torch.cuda.synchronize()
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    kv.lumen_kv_ckpt_plan(s, e, ws)
+    kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, dst, bt2, ws, back)
+    ok = bool(torch.equal(back, ck))
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    byts = 2.0 * rows * sh.token_row_bytes
+    return {"workload": w.name, "requests": w.num_reqs, "tokens": rows,
+            "bytes_each_way": rows * sh.token_row_bytes,
+            "plan_pack_us_median": float(np.median(pk)),
+            "plan_unpack_us_median": float(np.median(up)),
+            "plan_pack_us_p10_p90": [float(np.percentile(pk, q))
+                                     for q in (10, 90)],
+            "back_to_back_roundtrip_us": rt_us,
+            "back_to_back_GBps": gb(2 * byts) / (rt_us / 1e6),
+            "host_enqueue_us_per_call": host_us,
+            "roundtrip_ok": ok}
+
+
 def calibrate_copy(torch, mib):
     """A plain device-to-device copy of known size: read + write bytes are
     exactly 2 * mib MiB per launch, the scale for the FETCH_SIZE/WRITE_SIZE
@@ -1130,6 +1213,9 @@ def main():
                      "traffic": measured_traffic(dominant)},
         "workloads": {},
     }
+    if "tiny" in legs:
+        say("[bench] tiny leg (latency)")
+        out["workloads"]["tiny"] = rounded(tiny_leg(torch, kv, W))
     if "qwen" in legs:
         say("[bench] decode leg (qwen-gqa-hnd)")
         q = W.c5_qwen_hnd()

@@ -15,6 +15,7 @@ returned by lumen_kv_ckpt_status.
 from __future__ import annotations
 
 import ctypes
+import functools
 import os
 import re
 from typing import Optional
@@ -131,17 +132,23 @@ def layout(shape, num_blocks: int) -> lumen_kv_layout:
                            getattr(shape, "elem_bytes", 2), order)
 
 
+# Small checkpoints are launch-bound, so the per-call marshalling below is
+# kept cheap.
 def _stream_handle(stream: Optional[torch.cuda.Stream]):
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return ctypes.c_void_p(s.cuda_stream)
+    if stream is not None:
+        return ctypes.c_void_p(stream.cuda_stream)
+    # the raw handle of the current stream, without building a Stream object
+    return ctypes.c_void_p(torch._C._cuda_getCurrentRawStream(
+        torch.cuda.current_device()))
 
 
 def _dev(t: torch.Tensor, what: str, dtype=None) -> ctypes.c_void_p:
-    if not t.is_cuda:
+    d = t.get_device()
+    if d < 0:
         raise ValueError(f"{what} must be a device tensor")
-    if t.device.index != torch.cuda.current_device():
+    if d != torch.cuda.current_device():
         # the library launches on the current device
-        raise ValueError(f"{what} is on {t.device}, the current device is "
+        raise ValueError(f"{what} is on cuda:{d}, the current device is "
                          f"cuda:{torch.cuda.current_device()}")
     if not t.is_contiguous():
         raise ValueError(f"{what} must be contiguous")
@@ -181,6 +188,7 @@ def _check_tables(block_tables: torch.Tensor, num_reqs: int):
 
 # ------------------------------------------------------------- entry points
 
+@functools.lru_cache(maxsize=1024)
 def lumen_kv_ckpt_plan_workspace_bytes(num_reqs: int) -> int:
     return int(load_library().lumen_kv_ckpt_plan_workspace_bytes(num_reqs))
 

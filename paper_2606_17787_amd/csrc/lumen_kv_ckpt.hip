@@ -61,6 +61,10 @@ namespace {
 #ifndef LUMEN_KV_CKPT_WAVES_PER_CU
 #define LUMEN_KV_CKPT_WAVES_PER_CU 384
 #endif
+// Fewest bytes a wave of the copy grid is sized for (0: no such bound).
+#ifndef LUMEN_KV_CKPT_MIN_WAVE_BYTES
+#define LUMEN_KV_CKPT_MIN_WAVE_BYTES 4096
+#endif
 // Double-buffer the batches of a row segment (1) or not (0).
 #ifndef LUMEN_KV_CKPT_PIPELINE
 #define LUMEN_KV_CKPT_PIPELINE 1
@@ -83,6 +87,7 @@ constexpr int kWavesPerBlock = kBlockThreads / kWave;
 constexpr int kPlanThreads = 1024;
 constexpr int kUnroll = LUMEN_KV_CKPT_UNROLL;
 constexpr int kDefaultWavesPerCU = LUMEN_KV_CKPT_WAVES_PER_CU;
+constexpr int64_t kMinWaveBytes = LUMEN_KV_CKPT_MIN_WAVE_BYTES;
 
 // Workspace layout (device memory, caller-owned):
 //   WsHeader, then int64 prefix[R+1], int64 first_row[R], int32 start[R],
@@ -1049,11 +1054,19 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   // empty still costs a dispatch, so a checkpoint buffer sized to the rows
   // of the plan keeps small launches from paying for idle waves.
   int64_t waves = int64_t(dev->cus) * waves_per_cu();
-  const int64_t max_units =
-      (ckpt_rows < row_hi - row_lo ? ckpt_rows : row_hi - row_lo) *
-      int64_t(lay->num_layers);
+  const int64_t cap_rows = ckpt_rows < row_hi - row_lo ? ckpt_rows
+                                                       : row_hi - row_lo;
+  const int64_t max_units = cap_rows * int64_t(lay->num_layers);
   if (max_waves > 0 && max_waves < waves) waves = max_waves;
   if (max_units < waves) waves = max_units > 0 ? max_units : 1;
+  // Nor more waves than the buffer holds kMinWaveBytes pieces: where units
+  // are a few hundred bytes (one KV head per GPU), a wave per unit of a
+  // small checkpoint would leave the launch bound by wave dispatch.
+  if (kMinWaveBytes > 0 && cap_rows <= (INT64_MAX / 2) / g.row_bytes) {
+    const int64_t pieces = (cap_rows * g.row_bytes + kMinWaveBytes - 1) /
+                           kMinWaveBytes;
+    if (pieces < waves) waves = pieces > 0 ? pieces : 1;
+  }
   const unsigned blocks = unsigned((waves + kWavesPerBlock - 1) / kWavesPerBlock);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint8_t *in = static_cast<const uint8_t *>(src);

@@ -33,6 +33,54 @@ def test_tiny_workload_full_pack_and_restore():
     assert_same(gpu_path(*args), oracle_path(*args), "tiny")
 
 
+@pytest.mark.parametrize("which", ["shortest", "first", "pair"])
+def test_tp8_shape_small_checkpoints(which):
+    """Requests of the 70B TP=8 shard's shape (80 layers, one KV head: units
+    of 512 bytes) with checkpoint buffers sized to their rows, 16 KB to
+    200 MB, where the copy grid is bounded by one wavefront per 4 KiB of
+    checkpoint rather than one per unit: the full pack, the same rows
+    through a window (the token-major walk) and the restore into a second,
+    fragmented pool, against the oracle."""
+    w = W.c4_llama70b_tp8()
+    sh = w.shape
+    ctx = w.ends[0].astype(np.int64)
+    reqs = {"shortest": [int(np.argmin(ctx))], "first": [0],
+            "pair": [0, 1]}[which]
+    rng = np.random.default_rng(400 + len(reqs) + int(ctx[reqs[0]]))
+    lens = ctx[reqs]
+    s = np.zeros(len(reqs), np.int32)
+    if which == "pair":
+        s[1] = lens[1] // 3  # a request whose prefix was checkpointed before
+    e = lens.astype(np.int32)
+    pages = -(-lens // sh.block_size)
+    cols = int(pages.max())
+    nb = int(pages.sum()) + 5
+
+    def table():
+        perm = rng.permutation(nb).astype(np.int32)
+        bt = np.full((len(reqs), cols), -1, np.int32)
+        o = 0
+        for i, p in enumerate(pages):
+            bt[i, :p] = perm[o:o + p]
+            o += p
+        return bt
+
+    bt, bt2 = table(), table()
+    src = W.random_bits(rng, sh.pool_elems(nb))
+    dst = W.random_bits(rng, sh.pool_elems(nb))
+    args = (sh, nb, src, bt, s, e, nb, dst, bt2)
+    ref = oracle_path(*args)
+    assert_same(gpu_path(*args), ref, f"70B shape, {which}")
+    rows = int((e - s).sum())
+    ws = kv.new_workspace(len(reqs), dev())
+    kv.lumen_kv_ckpt_plan(h2d(s), h2d(e), ws)
+    win = torch.empty(rows * sh.token_row_elems, dtype=torch.int16,
+                      device=dev())
+    kv.lumen_kv_ckpt_pack_rows(sh, nb, h2d(src), h2d(bt), ws, 0, rows, win)
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    assert np.array_equal(d2h16(win).reshape(-1, sh.token_row_elems), ref[1])
+
+
 SHAPES = [
     CacheShape(1, 1, 8, 1, NHD), CacheShape(1, 1, 8, 1, HND),
     CacheShape(2, 2, 64, 2, NHD), CacheShape(2, 2, 64, 3, HND),

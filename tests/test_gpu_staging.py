@@ -444,3 +444,79 @@ def test_back_to_back_pipelines_share_one_ring():
         assert oracle.unpack(shape, nb, want_dst, bt2, steps[k][0],
                              steps[k][1], wants[k]) == 0
         assert np.array_equal(d2h_words(d_pool, 2), want_dst), k
+
+
+def test_pipelines_from_several_host_threads():
+    """Four host threads, each with its own streams, staging ring,
+    workspaces and pinned buffers, checkpoint to pinned host memory and
+    restore from it (through the staging ring, then directly) three times
+    over, at the same time.  The library's per-device state (device info,
+    the pipelines' event pool and ring table) is shared by all of them;
+    every host copy and restored pool must equal the oracle's."""
+    import threading
+
+    shape = CacheShape(3, 2, 64, 16, NHD)
+    rb = shape.token_row_bytes
+    jobs = []
+    for i in range(4):
+        nb, bt, bt2, s, e, src, dst = case(shape, 700 + i, R=17, max_tok=120)
+        st, want = oracle.pack(shape, nb, src, bt, s, e)
+        assert st == 0
+        want_dst = dst.copy()
+        assert oracle.unpack(shape, nb, want_dst, bt2, s, e, want) == 0
+        jobs.append(dict(nb=nb, total=int((e - s).sum()), dst=dst, want=want,
+                         want_dst=want_dst, d_src=h2d(src), d_bt=h2d(bt),
+                         d_bt2=h2d(bt2), d_s=h2d(s), d_e=h2d(e)))
+    torch.cuda.synchronize()
+    errors = []
+
+    def worker(i):
+        try:
+            j = jobs[i]
+            nb, total, want = j["nb"], j["total"], j["want"]
+            pack_s, copy_s, unpack_s = (torch.cuda.Stream(), torch.cuda.Stream(),
+                                        torch.cuda.Stream())
+            slots, slot_rows = 2, 7
+            staging = torch.empty(slots * slot_rows * rb, dtype=torch.uint8,
+                                  device=dev())
+            host = torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True)
+            ws = kv.new_workspace(j["d_s"].numel(), dev())
+            for it in range(3):
+                host.zero_()
+                torch.cuda.synchronize()
+                kv.lumen_kv_ckpt_plan(j["d_s"], j["d_e"], ws, stream=pack_s)
+                kv.lumen_kv_ckpt_pack_to_host(
+                    shape, nb, j["d_src"], j["d_bt"], ws, total, staging,
+                    slots, host, pack_stream=pack_s, copy_stream=copy_s)
+                copy_s.synchronize()
+                assert kv.lumen_kv_ckpt_status(ws, stream=pack_s) == 0
+                got = host.numpy().view(want.dtype).reshape(want.shape)
+                assert np.array_equal(got, want), (i, it, "ring pack")
+                for direct in (False, True):
+                    d_dst = h2d(j["dst"])
+                    torch.cuda.synchronize()
+                    kv.lumen_kv_ckpt_plan(j["d_s"], j["d_e"], ws,
+                                          stream=unpack_s)
+                    if direct:
+                        kv.lumen_kv_ckpt_unpack_from_host_direct(
+                            shape, nb, d_dst, j["d_bt2"], ws, host,
+                            stream=unpack_s)
+                    else:
+                        kv.lumen_kv_ckpt_unpack_from_host(
+                            shape, nb, d_dst, j["d_bt2"], ws, total, host,
+                            staging, slots, copy_stream=copy_s,
+                            unpack_stream=unpack_s)
+                    unpack_s.synchronize()
+                    assert kv.lumen_kv_ckpt_status(ws, stream=unpack_s) == 0
+                    assert np.array_equal(d2h_words(d_dst, shape.elem_bytes),
+                                          j["want_dst"]), (i, it, direct)
+        except BaseException as ex:  # reported by the main thread
+            errors.append((i, repr(ex)))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(4)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=90)
+    assert not any(t.is_alive() for t in threads), "a worker did not finish"
+    assert not errors, errors

@@ -61,9 +61,13 @@ namespace {
 #ifndef LUMEN_KV_CKPT_WAVES_PER_CU
 #define LUMEN_KV_CKPT_WAVES_PER_CU 384
 #endif
-// Fewest bytes a wave of the copy grid is sized for (0: no such bound).
+// Fewest bytes a wave of the copy grid is sized for (0: no such bound), and
+// the grid size per CU below which that bound does not cut.
 #ifndef LUMEN_KV_CKPT_MIN_WAVE_BYTES
 #define LUMEN_KV_CKPT_MIN_WAVE_BYTES 4096
+#endif
+#ifndef LUMEN_KV_CKPT_MIN_WAVES_PER_CU
+#define LUMEN_KV_CKPT_MIN_WAVES_PER_CU 16
 #endif
 // Double-buffer the batches of a row segment (1) or not (0).
 #ifndef LUMEN_KV_CKPT_PIPELINE
@@ -88,6 +92,7 @@ constexpr int kPlanThreads = 1024;
 constexpr int kUnroll = LUMEN_KV_CKPT_UNROLL;
 constexpr int kDefaultWavesPerCU = LUMEN_KV_CKPT_WAVES_PER_CU;
 constexpr int64_t kMinWaveBytes = LUMEN_KV_CKPT_MIN_WAVE_BYTES;
+constexpr int64_t kMinWavesPerCU = LUMEN_KV_CKPT_MIN_WAVES_PER_CU;
 
 // Workspace layout (device memory, caller-owned):
 //   WsHeader, then int64 prefix[R+1], int64 first_row[R], int32 start[R],
@@ -1061,10 +1066,14 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   if (max_units < waves) waves = max_units > 0 ? max_units : 1;
   // Nor more waves than the buffer holds kMinWaveBytes pieces: where units
   // are a few hundred bytes (one KV head per GPU), a wave per unit of a
-  // small checkpoint would leave the launch bound by wave dispatch.
+  // small checkpoint would leave the launch bound by wave dispatch.  Below
+  // kMinWavesPerCU waves per CU the bound does not cut, so that a tiny
+  // checkpoint still has enough waves in flight to hide memory latency.
   if (kMinWaveBytes > 0 && cap_rows <= (INT64_MAX / 2) / g.row_bytes) {
-    const int64_t pieces = (cap_rows * g.row_bytes + kMinWaveBytes - 1) /
-                           kMinWaveBytes;
+    int64_t pieces = (cap_rows * g.row_bytes + kMinWaveBytes - 1) /
+                     kMinWaveBytes;
+    const int64_t floor_waves = int64_t(dev->cus) * kMinWavesPerCU;
+    if (pieces < floor_waves) pieces = floor_waves;
     if (pieces < waves) waves = pieces > 0 ? pieces : 1;
   }
   const unsigned blocks = unsigned((waves + kWavesPerBlock - 1) / kWavesPerBlock);

@@ -18,6 +18,9 @@
 // different speeds on this chip, and short-lived ones let the hardware
 // dispatcher hand the remaining work to whichever CU frees a slot first,
 // where a grid of resident long-lived wavefronts ends on its slowest one.
+// Small checkpoints with short units get fewer, longer-lived wavefronts (at
+// least 4 KiB each, while that leaves 16 per CU), since there a wavefront
+// per unit makes wavefront dispatch the bound.
 // Inside its span a wavefront walks token rows in order: the
 // request, its block-table entry and the checkpoint row of each token are
 // wave-uniform and live in scalar registers; the 64 lanes then move the

@@ -16,6 +16,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <thread>
 #include <vector>
 
 #include "lumen_kv_ckpt.h"
@@ -274,7 +275,23 @@ int main() {
   for (const Case &c : cases)
     for (int rep = 0; rep < 3; ++rep) run_case(c, seed++, stream);
   HIP_OK(hipStreamDestroy(stream));
-  printf("abi conformance ok: %zu layouts x 3 seeds\n",
-         sizeof(cases) / sizeof(cases[0]));
+  // The same calls from four host threads at once, each on streams and
+  // buffers of its own: the library's per-device state (device properties,
+  // the pipelines' event pool and ring table) is shared between them.
+  constexpr int kThreads = 4;
+  std::vector<std::thread> threads;
+  for (int t = 0; t < kThreads; ++t)
+    threads.emplace_back([&cases, t] {
+      HIP_OK(hipSetDevice(0));
+      hipStream_t q = nullptr;
+      HIP_OK(hipStreamCreate(&q));
+      for (int rep = 0; rep < 2; ++rep)
+        for (const Case &c : cases)
+          run_case(c, 7000 + uint64_t(t) * 16 + uint64_t(rep), q);
+      HIP_OK(hipStreamDestroy(q));
+    });
+  for (std::thread &th : threads) th.join();
+  printf("abi conformance ok: %zu layouts x 3 seeds, then %d threads at once\n",
+         sizeof(cases) / sizeof(cases[0]), kThreads);
   return 0;
 }

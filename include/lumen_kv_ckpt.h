@@ -137,8 +137,9 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
  * be NULL only if it is empty (num_blocks, ckpt_rows or bt_cols is 0).
  *
  * Grid size.  The plan's row count lives in device memory, so the launch is
- * sized without it: 384 wavefronts per CU (LUMEN_KV_CKPT_WAVES_PER_CU in the
- * environment overrides this), but never more than one per (row, layer)
+ * sized without it: 384 wavefronts per CU, or 768 when a (row, layer) unit
+ * is shorter than 4 KiB (LUMEN_KV_CKPT_WAVES_PER_CU in the environment
+ * overrides both), but never more than one per (row, layer)
  * unit that ckpt_rows (or the row range of the _rows calls) could hold, nor
  * more than one per 4 KiB of it when that still leaves 16 per CU.  A
  * checkpoint buffer or window sized to the plan's rows keeps small steps

@@ -64,6 +64,13 @@ namespace {
 #ifndef LUMEN_KV_CKPT_WAVES_PER_CU
 #define LUMEN_KV_CKPT_WAVES_PER_CU 384
 #endif
+// The same for units (one token's K and V of one layer) shorter than 4 KiB,
+// unless the environment sets the count: measured on the head-major Qwen
+// steps (2 KiB units, about ten per wavefront at 384), 768 per CU gathers
+// 5% faster.
+#ifndef LUMEN_KV_CKPT_SHORT_UNIT_WAVES_PER_CU
+#define LUMEN_KV_CKPT_SHORT_UNIT_WAVES_PER_CU 768
+#endif
 // Fewest bytes a wave of the copy grid is sized for (0: no such bound), and
 // the grid size per CU below which that bound does not cut.
 #ifndef LUMEN_KV_CKPT_MIN_WAVE_BYTES
@@ -924,13 +931,15 @@ struct DeviceInfo {
 };
 DeviceInfo g_dev[kMaxDevices];
 
-int waves_per_cu() {
-  static int w = [] {
+int waves_per_cu(int64_t unit_bytes) {
+  static int env = [] {
     const char *e = getenv("LUMEN_KV_CKPT_WAVES_PER_CU");
-    int v = e ? atoi(e) : kDefaultWavesPerCU;
-    return v > 0 && v <= 4096 ? v : kDefaultWavesPerCU;
+    const int v = e ? atoi(e) : 0;
+    return v > 0 && v <= 4096 ? v : 0;
   }();
-  return w;
+  if (env > 0) return env;
+  return unit_bytes < 4096 ? LUMEN_KV_CKPT_SHORT_UNIT_WAVES_PER_CU
+                           : kDefaultWavesPerCU;
 }
 
 // Page-major pack for token-major caches whose per-token run is at most
@@ -1057,11 +1066,11 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   g.div_bs = make_fastdiv(uint32_t(bs));
 
   WsView v = ws_view(ws, num_reqs);
-  // Oversubscribed grid (LUMEN_KV_CKPT_WAVES_PER_CU per CU), never more
+  // Oversubscribed grid (waves_per_cu per CU, by unit size), never more
   // waves than the checkpoint buffer could hold units: a wave whose span is
   // empty still costs a dispatch, so a checkpoint buffer sized to the rows
   // of the plan keeps small launches from paying for idle waves.
-  int64_t waves = int64_t(dev->cus) * waves_per_cu();
+  int64_t waves = int64_t(dev->cus) * waves_per_cu(g.row_bytes / lay->num_layers);
   const int64_t cap_rows = ckpt_rows < row_hi - row_lo ? ckpt_rows
                                                        : row_hi - row_lo;
   const int64_t max_units = cap_rows * int64_t(lay->num_layers);

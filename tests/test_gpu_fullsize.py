@@ -1,14 +1,19 @@
 """The five workloads at their full sizes, on the GPU, in the launch
 configuration the benchmark times (the library's default grid).
 
-The oracle cannot hold 100+ GiB pools, so each check gathers the physical
-blocks a sampled set of requests touches into a compact host pool (a
+The oracle cannot hold 100+ GiB pools at once, so each check gathers the
+physical blocks a chunk of requests touches into a compact host pool (a
 consistent relabelling of blocks, which the oracle's pins show leaves the
 checkpoint unchanged), runs the oracle there and compares element by element
-with the rows the GPU wrote.  Properties that hold at any size cover the
-rest: restore after checkpoint round-trips over every request, and blocks no
-request names are left byte-identical.
+with the rows the GPU wrote.  Every checkpoint row of every workload is
+checked this way, and so is every restored token (packed back by the oracle
+from the restored pool).  Properties that hold at any size add to it:
+restore after checkpoint round-trips over every request on the GPU, and
+sampled blocks and slots no request names are left byte-identical.
 """
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 import torch
@@ -64,29 +69,11 @@ def compact_tables(bt, reqs, s, e, bs):
     return blocks, sub
 
 
-def oracle_rows(shape, pool_dev, nb, bt, reqs, s, e):
-    """Oracle checkpoint rows of the sampled requests, in sample order."""
-    blocks, sub = compact_tables(bt, reqs, s, e, shape.block_size)
-    host = gather_blocks(pool_dev, shape, nb, blocks)
-    st, ck = oracle.pack(shape, len(blocks), host, sub, s[reqs], e[reqs])
-    assert st == oracle.OK
-    return ck
-
-
 def gpu_rows(ck_dev, shape, first_row, reqs, s, e):
     rows = ck_dev.view(-1, shape.token_row_elems)
     out = [rows[int(first_row[r]):int(first_row[r]) + int(e[r] - s[r])]
            for r in reqs]
     return torch.cat(out).cpu().numpy().view(np.uint16)
-
-
-def check_pack_sample(shape, pool, nb, bt, s, e, ck, row_base, reqs, what):
-    _, first, _ = oracle.plan(s, e, row_base)
-    want = oracle_rows(shape, pool, nb, bt, reqs, s, e)
-    got = gpu_rows(ck, shape, first, reqs, s, e)
-    if not np.array_equal(got, want):
-        bad = np.argwhere(got != want)
-        raise AssertionError(f"{what}: {len(bad)} elements differ, first {bad[:3].tolist()}")
 
 
 def check_unpack_sample(shape, before, after, nb, bt, s, e, ck_rows_host,
@@ -126,6 +113,80 @@ def roundtrip_all(shape, nb, cache, bt, s, e, ck, row_base, chunk, what):
         assert torch.equal(tmp.view(-1, row_elems), ref), f"{what}: requests {r0}..{r1}"
 
 
+def check_all_rows(shape, pool, nb, bt, s, e, ck, row_base, what,
+                   chunk_bytes=1 << 30):
+    """Every checkpoint row of a packed plan against the oracle.  The token
+    ranges are cut into pieces, and consecutive pieces into chunks of about
+    chunk_bytes of rows.  Per chunk, the blocks its pieces touch are
+    gathered into a compact pinned host pool, the oracle (its C code, on the
+    host's threads, one run of pieces each) writes the chunk's rows into a
+    pinned buffer, and that buffer is compared on the device with the rows
+    the GPU wrote (one contiguous run of the checkpoint)."""
+    n = np.maximum(e.astype(np.int64) - s, 0)
+    if int(n.sum()) == 0:
+        return
+    row_elems = shape.token_row_elems
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    chunk_rows = max(threads, chunk_bytes // shape.token_row_bytes)
+    piece = max(1, chunk_rows // threads)
+    preq, ps, pe = [], [], []
+    for r in range(len(s)):
+        for t in range(int(s[r]), int(s[r]) + int(n[r]), piece):
+            preq.append(r)
+            ps.append(t)
+            pe.append(min(t + piece, int(s[r]) + int(n[r])))
+    preq = np.array(preq, np.int64)
+    ps = np.array(ps, np.int32)
+    pe = np.array(pe, np.int32)
+    plen = (pe - ps).astype(np.int64)
+    prow = row_base + np.concatenate([[0], np.cumsum(plen)[:-1]])
+    rows_dev = ck.view(-1, row_elems)
+    src_pin = out_pin = None
+    with ThreadPoolExecutor(threads) as ex:
+        i = 0
+        while i < len(preq):
+            j, rows = i, 0
+            while j < len(preq) and (j == i or rows + plen[j] <= chunk_rows):
+                rows += int(plen[j])
+                j += 1
+            blocks, sub = compact_tables(bt[preq[i:j]], np.arange(j - i),
+                                         ps[i:j], pe[i:j], shape.block_size)
+            idx = torch.from_numpy(np.asarray(blocks, np.int64)).to(DEV)
+            gathered = slab_view(pool, shape, nb).index_select(1, idx)
+            need = gathered.numel()
+            if src_pin is None or src_pin.numel() < need:
+                src_pin = torch.empty(need, dtype=torch.int16, pin_memory=True)
+            src_pin[:need].copy_(gathered.view(-1))
+            del gathered
+            host = src_pin[:need].numpy().view(np.uint16)
+            if out_pin is None or out_pin.numel() < rows * row_elems:
+                out_pin = torch.empty(rows * row_elems, dtype=torch.int16,
+                                      pin_memory=True)
+            out = out_pin[:rows * row_elems].numpy().view(np.uint16).reshape(
+                rows, row_elems)
+            cuts = np.linspace(i, j, threads + 1).astype(int)
+
+            def part(k):
+                a, b = cuts[k], cuts[k + 1]
+                if a >= b:
+                    return
+                lo = int(prow[a] - prow[i])
+                hi = lo + int(plen[a:b].sum())
+                st, _ = oracle.pack(shape, len(blocks), host, sub[a - i:b - i],
+                                    ps[a:b], pe[a:b], ckpt=out[lo:hi])
+                assert st == oracle.OK, (what, st)
+
+            list(ex.map(part, range(threads)))
+            want = out_pin[:rows * row_elems].to(DEV)
+            got = rows_dev[int(prow[i]):int(prow[i]) + rows].reshape(-1)
+            if not torch.equal(got, want):
+                bad = torch.nonzero(got != want)[:3].flatten().tolist()
+                raise AssertionError(
+                    f"{what}: rows {int(prow[i])}..{int(prow[i]) + rows}: "
+                    f"first differing elements {bad}")
+            i = j
+
+
 def sample(rng, R, k):
     return np.unique(np.concatenate([[0, R - 1], rng.choice(R, k, replace=False)]))
 
@@ -154,7 +215,6 @@ def test_incremental_full_size(make):
     bt = torch.from_numpy(w.block_tables).to(DEV)
     btd = torch.from_numpy(w.dst_block_tables).to(DEV)
     ws = kv.new_workspace(w.num_reqs, DEV)
-    full_check = {0, 1, w.num_steps - 1}
     for k in range(w.num_steps):
         s, e = w.starts[k], w.ends[k]
         kv.lumen_kv_ckpt_plan(torch.from_numpy(s).to(DEV),
@@ -162,16 +222,20 @@ def test_incremental_full_size(make):
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws, arena)
         kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, btd, ws, arena)
         assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK, f"step {k}"
-        reqs = (np.arange(w.num_reqs) if k in full_check
-                else sample(rng, w.num_reqs, 6))
-        check_pack_sample(sh, src, w.num_blocks, w.block_tables, s, e, arena,
-                          int(row_off[k]), reqs, f"{w.name} step {k}")
+        check_all_rows(sh, src, w.num_blocks, w.block_tables, s, e, arena,
+                       int(row_off[k]), f"{w.name} step {k}")
     say(f"[fullsize] {w.name}: restored pool re-packs to the checkpoint")
     # every restored token re-packs to its checkpoint row
     for k in range(w.num_steps):
         roundtrip_all(sh, w.dst_num_blocks, dst, w.dst_block_tables,
                       w.starts[k], w.ends[k],
                       arena, int(row_off[k]), 128, f"{w.name} step {k}")
+    # and, read back by the oracle, every restored token equals its row
+    # (every token is written by exactly one step)
+    for k in range(w.num_steps):
+        check_all_rows(sh, dst, w.dst_num_blocks, w.dst_block_tables,
+                       w.starts[k], w.ends[k], arena, int(row_off[k]),
+                       f"{w.name} restore of step {k}")
     # sampled requests' destination blocks, whole: written slots hold their
     # rows from every step, all other slots keep their bytes
     reqs = sample(rng, w.num_reqs, 14)
@@ -209,14 +273,10 @@ def test_restore_burst_full_size():
     slab_view(pool, sh, NB).copy_(fill.view(1, NB, 1).expand(
         sh.num_layers * 2, NB, slab_view(pool, sh, NB).shape[2]))
     ck = fill_random(max_rows * sh.token_row_elems, 13)
-    rng = np.random.default_rng(3)
     for wi, wv in enumerate(waves):
         s, e = w.starts[0][wv], w.ends[0][wv]
         bt = np.ascontiguousarray(w.dst_block_tables[wv])
         nrows = int(ctx[wv].sum())
-        reqs = sample(rng, len(wv), 3)
-        blocks, _ = compact_tables(bt, reqs, s, e, sh.block_size)
-        before = gather_blocks(pool, sh, NB, blocks)
         ws = kv.new_workspace(len(wv), DEV)
         kv.lumen_kv_ckpt_plan(torch.from_numpy(s).to(DEV),
                               torch.from_numpy(e).to(DEV), ws)
@@ -224,15 +284,27 @@ def test_restore_burst_full_size():
         kv.lumen_kv_ckpt_unpack(sh, NB, pool, torch.from_numpy(bt).to(DEV),
                                 ws, view)
         assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK
-        after = gather_blocks(pool, sh, NB, blocks)
-        _, first, _ = oracle.plan(s, e)
-        rows_h = gpu_rows(view, sh, first, reqs, s, e).reshape(-1, sh.token_row_elems)
-        check_unpack_sample(sh, before, after, NB, bt, s, e, rows_h, reqs,
-                            f"wave {wi}")
         roundtrip_all(sh, NB, pool, bt, s, e, view, 0, 4, f"wave {wi}")
+        # every restored token, read back by the oracle
+        check_all_rows(sh, pool, NB, bt, s, e, view, 0, f"wave {wi} restore")
+        sv = slab_view(pool, sh, NB)
+        # in every request's last block, the slots past its last token keep
+        # the block's constant (ranges start at token 0, so only the last
+        # block is partial)
+        assert sh.order == "NHD" and not s.any()
+        bs = sh.block_size
+        part = [i for i in range(len(wv)) if int(e[i]) % bs]
+        if part:
+            last = torch.from_numpy(np.array(
+                [bt[i, (int(e[i]) - 1) // bs] for i in part], np.int64)).to(DEV)
+            cut = torch.tensor([int(e[i]) % bs for i in part], device=DEV)
+            got = sv.index_select(1, last).view(sv.shape[0], len(part), bs, -1)
+            past = (torch.arange(bs, device=DEV).view(1, 1, bs, 1)
+                    >= cut.view(1, -1, 1, 1))
+            assert bool(((got == fill[last].view(1, -1, 1, 1)) | ~past).all()), \
+                f"wave {wi}: a slot past a request's last token changed"
         # occupied blocks keep their constant
         occ = torch.from_numpy(w.occupied).to(DEV)
-        sv = slab_view(pool, sh, NB)
         for c0 in range(0, occ.numel(), 1024):
             idx = occ[c0:c0 + 1024]
             got = sv.index_select(1, idx)
@@ -259,9 +331,9 @@ def test_tp8_shard_full_size_in_place():
     kv.lumen_kv_ckpt_pack(sh, w.num_blocks, pool,
                           torch.from_numpy(w.block_tables).to(DEV), ws, arena)
     assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK
+    check_all_rows(sh, pool, w.num_blocks, w.block_tables, s, e, arena, 0,
+                   "tp8 pack")
     reqs = sample(rng, w.num_reqs, 5)
-    check_pack_sample(sh, pool, w.num_blocks, w.block_tables, s, e, arena, 0,
-                      reqs, "tp8 pack")
     # restore in place under a fresh permutation of the same pool
     blocks, _ = compact_tables(w.dst_block_tables, reqs, s, e, sh.block_size)
     before = gather_blocks(pool, sh, w.num_blocks, blocks)

@@ -1,0 +1,57 @@
+"""Host-side logic of bench.py that needs no GPU: the hash that decides
+whether the committed HBM byte counters still describe the device code, and
+the refusal of more than one GPU."""
+import json
+import os
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_device_code_hash_tracks_the_kernels_only(tmp_path):
+    text = open(bench.KERNEL_SRC).read()
+    marker = "// " + "-" * 61 + " host side"
+    a, b = text.index("namespace {"), text.index(marker)
+    base = tmp_path / "base.hip"
+    base.write_text(text)
+    h0 = bench.device_code_sha256(str(base))
+    host_edit = tmp_path / "host.hip"
+    host_edit.write_text(text[:b] + marker + "\n// host-side note"
+                         + text[b + len(marker):])
+    assert bench.device_code_sha256(str(host_edit)) == h0
+    head_edit = tmp_path / "head.hip"
+    head_edit.write_text("// file header note\n" + text)
+    assert bench.device_code_sha256(str(head_edit)) == h0
+    kernel_edit = tmp_path / "kernel.hip"
+    mid = (a + b) // 2
+    kernel_edit.write_text(text[:mid] + "\n" + text[mid:])
+    assert bench.device_code_sha256(str(kernel_edit)) != h0
+
+
+def test_traffic_is_reported_only_for_the_profiled_code(tmp_path, monkeypatch):
+    text = open(bench.TRAFFIC_FILE).read()
+    data = json.loads(text[text.index("{", text.index("Machine-readable")):])
+    sha = bench.device_code_sha256()
+    for stored, expect in ((sha, True), ("0" * 64, False)):
+        data["device_code_sha256"] = stored
+        f = tmp_path / f"traffic_{expect}.txt"
+        f.write_text("counters\nMachine-readable:\n" + json.dumps(data))
+        monkeypatch.setattr(bench, "TRAFFIC_FILE", str(f))
+        got = bench.measured_traffic("pack")
+        if expect:
+            assert got == data["llama3-8b-decode"]["pack"]["traffic_bytes"]
+        else:
+            assert got is None
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "missing.txt"))
+    assert bench.measured_traffic("pack") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"),
+                        "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr

@@ -58,7 +58,7 @@ def draw(seed):
             waves, src, dst)
 
 
-@pytest.mark.parametrize("seed", range(60))
+@pytest.mark.parametrize("seed", range(400))
 def test_random_configuration_matches_oracle(seed):
     (rng, shape, R, nb, bt, bt2, s, e, error, per_request, row_base, waves,
      src, dst) = draw(seed)

@@ -132,3 +132,58 @@ def test_random_configuration_matches_oracle(seed):
         assert kv.lumen_kv_ckpt_status(ws) == 0
         got = np.concatenate([d2h_words(p, eb) for p in parts])
         assert np.array_equal(got.reshape(-1, re_), want_ck[row_base:])
+
+
+def draw_larger(seed):
+    """Serving-sized random shapes (up to 48 layers, 16 KV heads, head_dim
+    256, blocks of 64, 300 requests of up to 3,000 tokens), redrawn until
+    the pool fits 1.2 GB and the checkpoint 200 MB."""
+    rng = np.random.default_rng(9000 + seed)
+    while True:
+        shape = CacheShape(int(rng.integers(1, 49)), int(rng.integers(1, 17)),
+                           int(rng.choice([64, 128, 256])),
+                           int(rng.choice([8, 16, 32, 64])),
+                           HND if rng.random() < 0.5 else NHD)
+        R = int(rng.integers(1, 301))
+        ctx = rng.integers(1, 3001, R)
+        pages = -(-ctx // shape.block_size)
+        nb = int(pages.sum()) + int(rng.integers(0, 50))
+        s = np.where(rng.random(R) < 0.5, 0, rng.integers(0, ctx)).astype(np.int32)
+        e = np.minimum(s + rng.integers(0, 3001, R), ctx).astype(np.int32)
+        rows = int((e - s).sum())
+        if (shape.pool_elems(nb) * 2 <= 1.2e9
+                and rows * shape.token_row_bytes <= 2e8):
+            return rng, shape, R, nb, pages, s, e
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_larger_random_shape_matches_oracle(seed):
+    """Pack and restore of a serving-sized random shape, in the packed or
+    the per-request row mode, against the oracle.  At these sizes the copy
+    grid's spans cover several units and cross request boundaries, and the
+    unit sizes fall on both sides of the grid's 4 KiB threshold."""
+    from gpu_util import assert_same, gpu_path, oracle_path
+    rng, shape, R, nb, pages, s, e = draw_larger(seed)
+    cols = int(pages.max()) + int(rng.integers(0, 3))
+
+    def table():
+        perm = rng.permutation(nb).astype(np.int32)
+        bt = np.full((R, cols), -1, np.int32)
+        o = 0
+        for i, p in enumerate(pages):
+            bt[i, :p] = perm[o:o + p]
+            o += p
+        return bt
+
+    bt, bt2 = table(), table()
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    if rng.random() < 0.3:
+        n = (e - s).astype(np.int64)
+        kw = dict(req_row_base=np.concatenate([[0], np.cumsum(n + 2)[:-1]])
+                  - s + 1, ckpt_rows=int((n + 2).sum()) + 1)
+    else:
+        kw = dict(row_base=int(rng.integers(0, 5)))
+    args = (shape, nb, src, bt, s, e, nb, dst, bt2)
+    assert_same(gpu_path(*args, **kw), oracle_path(*args, **kw),
+                f"seed {seed}: {shape}, {R} requests")

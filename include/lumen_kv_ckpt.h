@@ -139,11 +139,11 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
  * Grid size.  The plan's row count lives in device memory, so the launch is
  * sized without it: 384 wavefronts per CU, or 768 when a (row, layer) unit
  * is shorter than 4 KiB (LUMEN_KV_CKPT_WAVES_PER_CU in the environment
- * overrides both), but never more than one per (row, layer)
- * unit that ckpt_rows (or the row range of the _rows calls) could hold, nor
- * more than one per 4 KiB of it when that still leaves 16 per CU.  A
- * checkpoint buffer or window sized to the plan's rows keeps small steps
- * free of idle wavefronts.
+ * overrides both), but never more than one per (row, layer) unit that
+ * ckpt_rows (or the row range of the _rows calls) could hold, nor more than
+ * one per 4 KiB of it when that still leaves 16 per CU.  A checkpoint
+ * buffer or window sized to the plan's rows keeps small steps free of idle
+ * wavefronts.
  *
  * Walk.  A pack of a token-major cache whose token runs (H*D*elem_bytes
  * bytes per layer and K/V) are at most 512 bytes is done page by page: whole

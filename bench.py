@@ -1016,7 +1016,7 @@ def tiny_leg(torch, kv, W, reps=200):
     so it reports latency: device us of plan + pack and of plan + unpack
     from HIP events around each pair with the stream drained in between,
     the same pairs back to back, and the host cost of enqueueing one call
-    through the binding.  Self-check: the restored tokens, packed again
+    through the binding, also with the calls prepared once (PreparedCall).  Self-check: the restored tokens, packed again
     from the destination pool, equal the checkpoint."""
     dev = torch.device("cuda:0")
     w = W.c1_tiny()
@@ -1057,6 +1057,20 @@ def tiny_leg(torch, kv, W, reps=200):
         return out
 
     pk, up = pair_us(pack), pair_us(unpack)
+    # the same calls prepared once: checks and marshalling outside the loop
+    p_plan = kv.prepare_plan(s, e, ws)
+    p_pack = kv.prepare_pack(sh, w.num_blocks, src, bt, ws, ck)
+    p_unpack = kv.prepare_unpack(sh, w.dst_num_blocks, dst, bt2, ws, ck)
+
+    def pack_prepared():
+        p_plan()
+        p_pack()
+
+    def unpack_prepared():
+        p_plan()
+        p_unpack()
+
+    pk_p, up_p = pair_us(pack_prepared), pair_us(unpack_prepared)
     torch.cuda.synchronize()
     a = TimingEvent()
     b = TimingEvent()
@@ -1073,6 +1087,11 @@ def tiny_leg(torch, kv, W, reps=200):
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws, ck)
     host_us = (time.perf_counter() - t0) * 1e6 / reps
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        p_pack()
+    host_p_us = (time.perf_counter() - t0) * 1e6 / reps
+    torch.cuda.synchronize()
     assert kv.lumen_kv_ckpt_status(ws) == 0
     kv.lumen_kv_ckpt_plan(s, e, ws)
     kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, dst, bt2, ws, back)
@@ -1088,6 +1107,9 @@ def tiny_leg(torch, kv, W, reps=200):
             "back_to_back_roundtrip_us": rt_us,
             "back_to_back_GBps": gb(2 * byts) / (rt_us / 1e6),
             "host_enqueue_us_per_call": host_us,
+            "prepared_plan_pack_us_median": float(np.median(pk_p)),
+            "prepared_plan_unpack_us_median": float(np.median(up_p)),
+            "prepared_host_enqueue_us_per_call": host_p_us,
             "roundtrip_ok": ok}
 
 

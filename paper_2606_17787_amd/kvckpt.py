@@ -203,10 +203,7 @@ def new_workspace(num_reqs: int, device=None) -> torch.Tensor:
     return torch.zeros(n, dtype=torch.uint8, device=device or "cuda")
 
 
-def lumen_kv_ckpt_plan(start: torch.Tensor, end: torch.Tensor,
-                       workspace: torch.Tensor, row_base: int = 0,
-                       req_row_base: Optional[torch.Tensor] = None,
-                       stream: Optional[torch.cuda.Stream] = None) -> None:
+def _plan_args(start, end, workspace, row_base, req_row_base):
     R = start.numel()
     if end.numel() != R:
         raise ValueError("start and end differ in length")
@@ -221,14 +218,23 @@ def lumen_kv_ckpt_plan(start: torch.Tensor, end: torch.Tensor,
         if req_row_base.numel() != R:
             raise ValueError("req_row_base must have one entry per request")
         pb = _dev(req_row_base, "req_row_base", torch.int64)
-    _check(load_library().lumen_kv_ckpt_plan(ps, pe, R, int(row_base), pb, pw,
-                                             _stream_handle(stream)),
+    return (ps, pe, R, int(row_base), pb, pw)
+
+
+def lumen_kv_ckpt_plan(start: torch.Tensor, end: torch.Tensor,
+                       workspace: torch.Tensor, row_base: int = 0,
+                       req_row_base: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None) -> None:
+    args = _plan_args(start, end, workspace, row_base, req_row_base)
+    _check(load_library().lumen_kv_ckpt_plan(*args, _stream_handle(stream)),
            "lumen_kv_ckpt_plan")
 
 
-def _copy(name: str, shape, num_blocks: int, cache: torch.Tensor,
-          block_tables: torch.Tensor, workspace: torch.Tensor,
-          ckpt: torch.Tensor, stream):
+def _copy_args(shape, num_blocks: int, cache: torch.Tensor,
+               block_tables: torch.Tensor, workspace: torch.Tensor,
+               ckpt: torch.Tensor):
+    """(layout struct, argument tuple without the stream) of a pack or
+    unpack; the struct must outlive every use of the tuple."""
     R = block_tables.shape[0] if block_tables.dim() == 2 else -1
     _check_tables(block_tables, R)
     _check_cache(shape, num_blocks, cache, "cache")
@@ -241,11 +247,78 @@ def _copy(name: str, shape, num_blocks: int, cache: torch.Tensor,
                          f"{_elem_bytes(shape)}-byte elements")
     rows = ckpt.numel() // _row_elems(shape)
     lay = layout(shape, num_blocks)
-    f = getattr(load_library(), name)
-    _check(f(ctypes.byref(lay), _dev(cache, "cache"),
-             _dev(block_tables, "block_tables", torch.int32),
-             block_tables.shape[1], R, _dev(workspace, "workspace"),
-             _dev(ckpt, "ckpt"), rows, _stream_handle(stream)), name)
+    return lay, (ctypes.byref(lay), _dev(cache, "cache"),
+                 _dev(block_tables, "block_tables", torch.int32),
+                 block_tables.shape[1], R, _dev(workspace, "workspace"),
+                 _dev(ckpt, "ckpt"), rows)
+
+
+def _copy(name: str, shape, num_blocks: int, cache: torch.Tensor,
+          block_tables: torch.Tensor, workspace: torch.Tensor,
+          ckpt: torch.Tensor, stream):
+    lay, args = _copy_args(shape, num_blocks, cache, block_tables, workspace,
+                           ckpt)
+    _check(getattr(load_library(), name)(*args, _stream_handle(stream)), name)
+
+
+class PreparedCall:
+    """One entry point with its arguments checked and marshalled once.
+
+    A serving loop issues the same plan, pack and unpack on the same
+    buffers every step (the token ranges are device tensors it rewrites in
+    place), and for small checkpoints the per-call checks cost as much as
+    the launch.  Calling the object enqueues the entry point on `stream` or
+    the current stream, with no checks but the device's.  It keeps the
+    tensors alive; they must keep their storage (no resize or reallocation)
+    for as long as the object is used."""
+    __slots__ = ("_fn", "_args", "_name", "_device", "_keep")
+
+    def __init__(self, name: str, args: tuple, keep: tuple):
+        self._fn = getattr(load_library(), name)
+        self._args = args
+        self._name = name
+        self._device = torch.cuda.current_device()
+        self._keep = keep
+
+    def __call__(self, stream: Optional[torch.cuda.Stream] = None) -> None:
+        if torch.cuda.current_device() != self._device:
+            raise ValueError(f"{self._name} was prepared on "
+                             f"cuda:{self._device}; the current device is "
+                             f"cuda:{torch.cuda.current_device()}")
+        h = (stream.cuda_stream if stream is not None else
+             torch._C._cuda_getCurrentRawStream(self._device))
+        _check(self._fn(*self._args, ctypes.c_void_p(h)), self._name)
+
+
+def prepare_plan(start: torch.Tensor, end: torch.Tensor,
+                 workspace: torch.Tensor, row_base: int = 0,
+                 req_row_base: Optional[torch.Tensor] = None) -> PreparedCall:
+    """lumen_kv_ckpt_plan with its arguments checked once; see PreparedCall."""
+    return PreparedCall("lumen_kv_ckpt_plan",
+                        _plan_args(start, end, workspace, row_base,
+                                   req_row_base),
+                        (start, end, workspace, req_row_base))
+
+
+def prepare_pack(shape, num_blocks: int, cache: torch.Tensor,
+                 block_tables: torch.Tensor, workspace: torch.Tensor,
+                 ckpt: torch.Tensor) -> PreparedCall:
+    """lumen_kv_ckpt_pack with its arguments checked once; see PreparedCall."""
+    lay, args = _copy_args(shape, num_blocks, cache, block_tables, workspace,
+                           ckpt)
+    return PreparedCall("lumen_kv_ckpt_pack", args,
+                        (lay, cache, block_tables, workspace, ckpt))
+
+
+def prepare_unpack(shape, num_blocks: int, cache: torch.Tensor,
+                   block_tables: torch.Tensor, workspace: torch.Tensor,
+                   ckpt: torch.Tensor) -> PreparedCall:
+    """lumen_kv_ckpt_unpack with its arguments checked once; see
+    PreparedCall."""
+    lay, args = _copy_args(shape, num_blocks, cache, block_tables, workspace,
+                           ckpt)
+    return PreparedCall("lumen_kv_ckpt_unpack", args,
+                        (lay, cache, block_tables, workspace, ckpt))
 
 
 def lumen_kv_ckpt_pack(shape, num_blocks: int, cache: torch.Tensor,

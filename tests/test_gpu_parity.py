@@ -33,6 +33,55 @@ def test_tiny_workload_full_pack_and_restore():
     assert_same(gpu_path(*args), oracle_path(*args), "tiny")
 
 
+def test_prepared_calls_match_the_oracle():
+    """Plan, pack and unpack prepared once and issued twice on the same
+    buffers, with the token ranges rewritten in place in between (a serving
+    loop's use): each round equals the oracle, and the plain calls."""
+    w = W.c1_tiny()
+    sh = w.shape
+    rng = np.random.default_rng(202)
+    src = W.random_bits(rng, sh.pool_elems(w.num_blocks))
+    dst = W.random_bits(rng, sh.pool_elems(w.dst_num_blocks))
+    s0, e0 = w.starts[0], w.ends[0]
+    s1 = (s0 + rng.integers(0, 40, len(s0))).astype(np.int32)
+    e1 = np.maximum(s1, e0 - rng.integers(0, 40, len(e0))).astype(np.int32)
+    rows = int(max((e0 - s0).sum(), (e1 - s1).sum()))
+    d_s, d_e = h2d(s0), h2d(e0)
+    d_src, d_dst = h2d(src), h2d(dst)
+    ck = torch.zeros(rows * sh.token_row_elems, dtype=torch.int16,
+                     device=dev())
+    ws = kv.new_workspace(len(s0), dev())
+    plan = kv.prepare_plan(d_s, d_e, ws)
+    pack = kv.prepare_pack(sh, w.num_blocks, d_src, h2d(w.block_tables), ws,
+                           ck)
+    unpack = kv.prepare_unpack(sh, w.dst_num_blocks, d_dst,
+                               h2d(w.dst_block_tables), ws, ck)
+    want_dst = dst.copy()
+    for s, e in ((s0, e0), (s1, e1)):
+        d_s.copy_(torch.from_numpy(s))
+        d_e.copy_(torch.from_numpy(e))
+        plan()
+        pack()
+        unpack()
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+        n = int((e - s).sum())
+        st, want = oracle.pack(sh, w.num_blocks, src, w.block_tables, s, e)
+        assert st == oracle.OK
+        assert oracle.unpack(sh, w.dst_num_blocks, want_dst,
+                             w.dst_block_tables, s, e, want) == oracle.OK
+        got = d2h16(ck)[:n * sh.token_row_elems].reshape(want.shape)
+        assert np.array_equal(got, want)
+        assert np.array_equal(d2h16(d_dst), want_dst)
+        # the plain call on the same ranges writes the same rows
+        ck2 = torch.zeros_like(ck)
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws)
+        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, d_src, h2d(w.block_tables),
+                              ws, ck2)
+        assert kv.lumen_kv_ckpt_status(ws) == 0
+        assert torch.equal(ck2[:n * sh.token_row_elems],
+                           ck[:n * sh.token_row_elems])
+
+
 @pytest.mark.parametrize("which", ["shortest", "first", "pair"])
 def test_tp8_shape_small_checkpoints(which):
     """Requests of the 70B TP=8 shard's shape (80 layers, one KV head: units

@@ -592,28 +592,30 @@ pack_pages_kernel(const uint8_t *__restrict__ cache, uint8_t *__restrict__ ckpt,
     const int64_t t_hi = min(e, (j + 1) * g.block_size);
     const int32_t nt = int32_t(t_hi - t_lo);
     const int64_t row0 = first_row[r] + (t_lo - s) - g.win_first;
-    int code = LUMEN_OK;
-    int32_t b = -1;
+    // The item's rows are consecutive: the ones inside the buffer are the
+    // tokens [ta, tb) of the page; the others are CAPACITY errors and only
+    // they are skipped.
+    const int64_t ta64 = row0 < 0 ? -row0 : 0;
+    const int64_t room = g.ckpt_rows - row0;
+    const int32_t ta = int32_t(min(ta64, int64_t(nt)));
+    const int32_t tb = int32_t(max(min(room, int64_t(nt)), int64_t(ta)));
     if (j >= g.bt_cols) {
-      code = LUMEN_ERR_RANGE;
-    } else {
-      b = block_tables[int64_t(r) * g.bt_cols + j];
-      if (b < 0 || b >= g.num_blocks)
-        code = LUMEN_ERR_BLOCK_ID;
-      else if (row0 < 0 || row0 + nt > g.ckpt_rows)
-        code = LUMEN_ERR_CAPACITY;
-    }
-    if (code != LUMEN_OK) {
-      record_error(err, code);
+      record_error(err, LUMEN_ERR_RANGE);
       continue;
     }
+    const int32_t b = block_tables[int64_t(r) * g.bt_cols + j];
+    if (b < 0 || b >= g.num_blocks) {
+      record_error(err, LUMEN_ERR_BLOCK_ID);
+      continue;
+    }
+    if (ta > 0 || tb < nt) record_error(err, LUMEN_ERR_CAPACITY);
     const int64_t blk = int64_t(b) * g.block_bytes +
                         (t_lo - j * g.block_size) * int64_t(tok);
-    const int32_t nv = nt * vpt;  // vectors of one K or V run
+    const int32_t nv = tb * vpt;  // vectors of the K (or V) run to copy
     for (int32_t l = l_first; l < l_end; ++l) {
     const uint8_t *k_run = cache + int64_t(l * 2) * g.slab_bytes + blk;
     const uint8_t *v_run = k_run + g.slab_bytes;
-    for (int32_t v0 = 0; v0 < nv; v0 += kWave * kUnroll) {
+    for (int32_t v0 = ta * vpt; v0 < nv; v0 += kWave * kUnroll) {
       uint4 ka[kUnroll], va[kUnroll];
 #pragma unroll
       for (int k = 0; k < kUnroll; ++k) {

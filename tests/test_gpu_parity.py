@@ -13,7 +13,8 @@ import paper_2606_17787_amd.kvckpt as kv
 from paper_2606_17787_amd import workloads as W
 from paper_2606_17787_amd.workloads import CacheShape, HND, NHD
 
-from gpu_util import assert_same, gpu_path, oracle_path, h2d, d2h16, dev
+from gpu_util import (SENTINEL, assert_same, gpu_path, oracle_path, h2d,
+                      d2h16, dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -240,6 +241,93 @@ def test_device_error_codes_match_oracle(case):
     st_g, _, _ = gpu_path(shape, nb, src, np.array([[0, 1, 2], [3, 4, 5]],
                                                    np.int32), [0, 0], [1, 1])
     assert st_g == kv.LUMEN_OK
+
+
+# One shape per walk of the copy kernels: 32-byte token runs (the full pack
+# takes the page-major walk), 1 KiB runs (token-major walk) and a head-major
+# cache.
+ERROR_WALK_SHAPES = {
+    "nhd-page-major": CacheShape(2, 2, 8, 4, NHD),
+    "nhd-token-major": CacheShape(2, 8, 64, 4, NHD),
+    "hnd": CacheShape(2, 2, 8, 4, HND),
+}
+
+
+def _valid_token_rows(shape, nb, bt, s, e, rows, base, rb):
+    """(request, token, checkpoint row) of every token that passes the
+    per-row checks the header documents, in their order: page inside the
+    table, entry inside the pool, row inside the buffer.  Requests whose
+    range is invalid contribute no rows."""
+    out, run = [], int(base)
+    for r in range(len(s)):
+        if s[r] < 0 or e[r] < s[r]:
+            continue
+        first = (int(rb[r]) + int(s[r])) if rb is not None else run
+        run += int(e[r]) - int(s[r])
+        for t in range(int(s[r]), int(e[r])):
+            j = t // shape.block_size
+            crow = first + (t - int(s[r]))
+            if j >= bt.shape[1] or not 0 <= bt[r, j] < nb:
+                continue
+            if 0 <= crow < rows:
+                out.append((r, t, crow))
+    return out
+
+
+@pytest.mark.parametrize("walk", list(ERROR_WALK_SHAPES))
+@pytest.mark.parametrize("case", range(len(ERROR_CASES)))
+def test_error_inputs_still_copy_every_valid_row(case, walk):
+    """On data-dependent errors only the offending token rows are skipped:
+    every other row of the pack equals the oracle's pack of that token
+    alone, rows no valid token names keep their sentinel, and the unpack
+    writes exactly the valid tokens' slots, for each walk of the kernels."""
+    s, e, bt, rows, base, rb = ERROR_CASES[case]
+    shape = ERROR_WALK_SHAPES[walk]
+    nb = 8
+    bt = np.array(bt if bt is not None else [[0, 1, 2], [3, 4, -1]], np.int32)
+    s, e = np.asarray(s, np.int32), np.asarray(e, np.int32)
+    rng = np.random.default_rng(1000 + case)
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    ck_in = W.random_bits(rng, rows * shape.token_row_elems)
+    valid = _valid_token_rows(shape, nb, bt, s, e, rows, base, rb)
+
+    want_ck = np.full((rows, shape.token_row_elems), SENTINEL, np.uint16)
+    want_dst = dst.copy()
+    named = {}  # checkpoint row -> the rows of the tokens naming it
+    for r, t, crow in valid:
+        st, one = oracle.pack(shape, nb, src, bt[r:r + 1], [t], [t + 1])
+        assert st == oracle.OK
+        want_ck[crow] = one[0]
+        named.setdefault(crow, []).append(one[0])
+        assert oracle.unpack(shape, nb, want_dst, bt[r:r + 1], [t], [t + 1],
+                             ck_in.reshape(rows, -1)[crow:crow + 1]) == 0
+    st_o, _ = oracle.pack(shape, nb, src, bt, s, e, base, rb,
+                          ckpt=np.zeros((rows + 8, shape.token_row_elems),
+                                        np.uint16), ckpt_rows=rows)
+
+    ws = kv.new_workspace(len(s), dev())
+    d_rb = None if rb is None else h2d(np.asarray(rb, np.int64))
+    d_s, d_e, d_bt = h2d(s), h2d(e), h2d(bt)
+    ck = h2d(np.full(rows * shape.token_row_elems, SENTINEL, np.uint16))
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, base, d_rb)
+    kv.lumen_kv_ckpt_pack(shape, nb, h2d(src), d_bt, ws, ck)
+    assert kv.lumen_kv_ckpt_status(ws) == st_o
+    got_ck = d2h16(ck).reshape(rows, -1)
+    # Overlapping per-request regions (a caller error): the writers of a row
+    # two tokens name race, so each element holds one of theirs.
+    for crow, cands in named.items():
+        if len(cands) > 1:
+            assert np.logical_or.reduce([got_ck[crow] == c for c in cands]).all()
+            want_ck[crow] = got_ck[crow]
+    assert np.array_equal(got_ck, want_ck), \
+        f"{walk}: pack rows differ from the oracle's valid rows"
+    d_dst = h2d(dst)
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, base, d_rb)
+    kv.lumen_kv_ckpt_unpack(shape, nb, d_dst, d_bt, ws, h2d(ck_in))
+    assert kv.lumen_kv_ckpt_status(ws) == st_o
+    assert np.array_equal(d2h16(d_dst), want_dst), \
+        f"{walk}: unpack wrote other slots than the valid tokens'"
 
 
 def test_status_clears_the_error_word():

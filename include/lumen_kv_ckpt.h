@@ -88,6 +88,13 @@ extern "C" {
 #define LUMEN_ERR_CAPACITY (-7)    /* checkpoint row outside [0, ckpt_rows); host libraries: out of host memory */
 #define LUMEN_ERR_DUP_BLOCK (-8)   /* validate mode: a block named by two
                                       pages that an unpack would write */
+#define LUMEN_ERR_TOO_MANY (-9)    /* lumen_kv_ckpt_pack_noalloc: more than
+                                      LUMEN_KV_CKPT_NOALLOC_MAX_REQS requests */
+
+/* Most requests lumen_kv_ckpt_pack_noalloc takes in one call. */
+#ifndef LUMEN_KV_CKPT_NOALLOC_MAX_REQS
+#define LUMEN_KV_CKPT_NOALLOC_MAX_REQS 16384
+#endif
 
 #define LUMEN_CACHE_NHD 0
 #define LUMEN_CACHE_HND 1
@@ -154,6 +161,32 @@ int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
                        const int32_t *d_block_tables, int32_t bt_cols,
                        int32_t num_reqs, void *d_workspace, void *d_ckpt,
                        int64_t ckpt_rows, lumen_stream_t stream);
+
+/* Plan and pack in one call that allocates nothing, for callers that cannot
+ * allocate device memory or be handed a workspace: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  The same
+ * as lumen_kv_ckpt_plan(d_start, d_end, num_reqs, row_base, d_req_row_base,
+ * ws, stream) followed by lumen_kv_ckpt_pack(layout, d_cache,
+ * d_block_tables, bt_cols, num_reqs, ws, d_ckpt, ckpt_rows, stream), with
+ * the workspace ws replaced by a device array the library holds (one per
+ * GPU, about 460 KB, kept until the process ends) and the status written to
+ * d_status (caller-owned device int32, 4-byte aligned): the most negative
+ * code the plan and the pack recorded, 0 if none, once the stream has
+ * passed the call.  The caller still owns every input and output.
+ * Calls no allocating routine.  num_reqs above
+ * LUMEN_KV_CKPT_NOALLOC_MAX_REQS returns LUMEN_ERR_TOO_MANY and enqueues
+ * nothing.  Every call on a GPU shares that GPU's array: calls that overlap
+ * on one GPU (two streams, or two host threads, with no ordering between
+ * them) race and give undefined results; calls ordered on one stream are
+ * safe, since each call's plan rewrites what its pack reads. */
+int lumen_kv_ckpt_pack_noalloc(const lumen_kv_layout *layout,
+                               const void *d_cache,
+                               const int32_t *d_block_tables, int32_t bt_cols,
+                               const int32_t *d_start, const int32_t *d_end,
+                               int32_t num_reqs, int64_t row_base,
+                               const int64_t *d_req_row_base, void *d_ckpt,
+                               int64_t ckpt_rows, int32_t *d_status,
+                               lumen_stream_t stream);
 
 /* Restore scatter (Sec. 4.3, loading checkpointed pages into GPU memory):
  * the inverse of lumen_kv_ckpt_pack under d_block_tables (usually freshly

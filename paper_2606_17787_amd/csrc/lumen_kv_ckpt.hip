@@ -141,7 +141,7 @@ WsView ws_view(void *ws, int32_t R) {
   return v;
 }
 
-size_t ws_bytes(int32_t R) {
+constexpr size_t ws_bytes(int32_t R) {
   size_t off = sizeof(WsHeader);
   off = align16(off + sizeof(int64_t) * (size_t(R) + 1));
   off = align16(off + sizeof(int64_t) * size_t(R));
@@ -651,7 +651,8 @@ pack_pages_kernel(const uint8_t *__restrict__ cache, uint8_t *__restrict__ ckpt,
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const int32_t *__restrict__ d_start, const int32_t *__restrict__ d_end,
     int32_t R, int64_t row_base, const int64_t *__restrict__ req_row_base,
-    WsHeader *hdr, int64_t *prefix, int64_t *first_row, int32_t *start) {
+    WsHeader *hdr, int64_t *prefix, int64_t *first_row, int32_t *start,
+    int32_t *err) {
   constexpr int kWaves = kPlanThreads / kWave;
   __shared__ int64_t wave_sum[kWaves];
   __shared__ int bad;
@@ -703,7 +704,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     prefix[R] = total;
     hdr->total_rows = total;
     hdr->num_reqs = R;
-    hdr->err = bad ? LUMEN_ERR_RANGE : LUMEN_OK;
+    hdr->err = LUMEN_OK;
+    *err = bad ? LUMEN_ERR_RANGE : LUMEN_OK;  // the header's word, or the
+                                              // caller's status word
   }
 }
 
@@ -899,6 +902,15 @@ __global__ __launch_bounds__(kPlanThreads) void draft_free_kernel(
 // ------------------------------------------------------------- host side
 
 constexpr int kMaxDevices = 64;
+
+// Plan workspace of lumen_kv_ckpt_pack_noalloc, for callers that cannot
+// allocate: one copy per device, held until the process ends, sized for
+// kNoAllocMaxReqs requests.  Host code must not use this name as an address
+// (it is a host-side stand-in); each device's address comes from
+// hipGetSymbolAddress at that device's set-up.
+constexpr int32_t kNoAllocMaxReqs = LUMEN_KV_CKPT_NOALLOC_MAX_REQS;
+constexpr size_t kScratchBytes = ws_bytes(kNoAllocMaxReqs);
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 constexpr int32_t kMaxSlots = 64;  // ring slots of a staging pipeline
 constexpr size_t kMaxRings = 16;   // staging rings remembered per device
 // Direct host copies: default and largest workgroup counts.  Measured on
@@ -930,6 +942,8 @@ struct DeviceInfo {
   };
   std::vector<Ring> rings;
   size_t ring_next = 0;  // entry reused once kMaxRings are known
+  // This device's copy of `scratch` (null if its address could not be had).
+  void *scratch = nullptr;
 };
 DeviceInfo g_dev[kMaxDevices];
 
@@ -983,6 +997,12 @@ int current_device(DeviceInfo **info) {
     hipEvent_t ev = nullptr;
     if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess)
       d.order_event = ev;
+    // Device `dev` is current here, so this is its copy of the array.
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) == hipSuccess)
+      d.scratch = ptr;
+    else
+      (void)hipGetLastError();  // only the allocation-free call needs it
   });
   if (d.cus <= 0 || !d.order_event) return LUMEN_ERR_HIP;
   *info = &d;
@@ -1014,6 +1034,18 @@ int check_layout(const lumen_kv_layout *lay) {
   return LUMEN_OK;
 }
 
+// A buffer may be null only when it is empty; the device checks then keep
+// every access away from it.
+int check_copy_buffers(const lumen_kv_layout *lay, const void *cache,
+                       const void *ckpt, const int32_t *bt, int32_t bt_cols,
+                       int64_t ckpt_rows) {
+  if ((!cache && lay->num_blocks > 0) || (!ckpt && ckpt_rows > 0) ||
+      (!bt && bt_cols > 0))
+    return LUMEN_ERR_INVALID_ARG;
+  if (!aligned16(cache) || !aligned16(ckpt)) return LUMEN_ERR_MISALIGNED;
+  return LUMEN_OK;
+}
+
 // max_waves > 0 caps the grid (a copy whose checkpoint side is host memory
 // across the host link needs a few hundred wavefronts, not the HBM grid) and
 // keeps the token-major walk, whose checkpoint accesses are sequential.
@@ -1021,7 +1053,7 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
                 void *dst, const int32_t *bt, int32_t bt_cols,
                 int32_t num_reqs, void *ws, int64_t row_lo, int64_t row_hi,
                 int64_t win_first, int64_t ckpt_rows, lumen_stream_t stream,
-                int64_t max_waves = 0) {
+                int64_t max_waves = 0, int32_t *err_word = nullptr) {
   int st = check_layout(lay);
   if (st != LUMEN_OK) return st;
   if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0) return LUMEN_ERR_INVALID_ARG;
@@ -1029,14 +1061,9 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   if (!ws) return LUMEN_ERR_INVALID_ARG;
   if (!aligned16(ws)) return LUMEN_ERR_MISALIGNED;
   if (num_reqs == 0 || row_hi == row_lo) return LUMEN_OK;
-  // A buffer may be null only when it is empty; the device checks then keep
-  // every access away from it.
-  const void *cache = pack ? src : dst;
-  const void *ckpt = pack ? dst : src;
-  if ((!cache && lay->num_blocks > 0) || (!ckpt && ckpt_rows > 0) ||
-      (!bt && bt_cols > 0))
-    return LUMEN_ERR_INVALID_ARG;
-  if (!aligned16(src) || !aligned16(dst)) return LUMEN_ERR_MISALIGNED;
+  st = check_copy_buffers(lay, pack ? src : dst, pack ? dst : src, bt,
+                          bt_cols, ckpt_rows);
+  if (st != LUMEN_OK) return st;
   DeviceInfo *dev = nullptr;
   st = current_device(&dev);
   if (st != LUMEN_OK) return st;
@@ -1068,6 +1095,7 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   g.div_bs = make_fastdiv(uint32_t(bs));
 
   WsView v = ws_view(ws, num_reqs);
+  int32_t *err = err_word ? err_word : &v.hdr->err;
   // Oversubscribed grid (waves_per_cu per CU, by unit size), never more
   // waves than the checkpoint buffer could hold units: a wave whose span is
   // empty still costs a dispatch, so a checkpoint buffer sized to the rows
@@ -1101,25 +1129,25 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
                        lay->block_size);
     hipLaunchKernelGGL(pack_pages_kernel, dim3(blocks), dim3(kBlockThreads),
                        0, s, in, out, bt, v.hdr, v.prefix, v.first_row,
-                       v.start, v.items, &v.hdr->err, g);
+                       v.start, v.items, err, g);
   } else if (pack) {
     if (hnd)
       hipLaunchKernelGGL((copy_rows_kernel<true, true>), dim3(blocks),
                          dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+                         v.prefix, v.first_row, v.start, err, g);
     else
       hipLaunchKernelGGL((copy_rows_kernel<true, false>), dim3(blocks),
                          dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+                         v.prefix, v.first_row, v.start, err, g);
   } else {
     if (hnd)
       hipLaunchKernelGGL((copy_rows_kernel<false, true>), dim3(blocks),
                          dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+                         v.prefix, v.first_row, v.start, err, g);
     else
       hipLaunchKernelGGL((copy_rows_kernel<false, false>), dim3(blocks),
                          dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, &v.hdr->err, g);
+                         v.prefix, v.first_row, v.start, err, g);
   }
   return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
 }
@@ -1274,7 +1302,7 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0,
                      static_cast<hipStream_t>(stream), d_start, d_end,
                      num_reqs, row_base, d_req_row_base, v.hdr, v.prefix,
-                     v.first_row, v.start);
+                     v.first_row, v.start, &v.hdr->err);
   return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
 }
 
@@ -1285,6 +1313,46 @@ int lumen_kv_ckpt_pack(const lumen_kv_layout *layout, const void *d_cache,
   return launch_copy(true, layout, d_cache, d_ckpt, d_block_tables, bt_cols,
                      num_reqs, d_workspace, 0, INT64_MAX, 0, ckpt_rows,
                      stream);
+}
+
+int lumen_kv_ckpt_pack_noalloc(const lumen_kv_layout *layout,
+                               const void *d_cache,
+                               const int32_t *d_block_tables, int32_t bt_cols,
+                               const int32_t *d_start, const int32_t *d_end,
+                               int32_t num_reqs, int64_t row_base,
+                               const int64_t *d_req_row_base, void *d_ckpt,
+                               int64_t ckpt_rows, int32_t *d_status,
+                               lumen_stream_t stream) {
+  // Every host check comes before the first launch, so that an argument
+  // error enqueues nothing.
+  int st = check_layout(layout);
+  if (st != LUMEN_OK) return st;
+  if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0 || !d_status)
+    return LUMEN_ERR_INVALID_ARG;
+  if (num_reqs > kNoAllocMaxReqs) return LUMEN_ERR_TOO_MANY;
+  if (reinterpret_cast<uintptr_t>(d_status) & 3) return LUMEN_ERR_MISALIGNED;
+  if (num_reqs > 0) {
+    if (!d_start || !d_end) return LUMEN_ERR_INVALID_ARG;
+    st = check_copy_buffers(layout, d_cache, d_ckpt, d_block_tables, bt_cols,
+                            ckpt_rows);
+    if (st != LUMEN_OK) return st;
+  }
+  DeviceInfo *dev = nullptr;
+  st = current_device(&dev);
+  if (st != LUMEN_OK) return st;
+  if (!dev->scratch) return LUMEN_ERR_HIP;
+  // The plan overwrites everything the pack reads from the scratch (its
+  // header and per-request arrays) and the status word, so nothing left by
+  // an earlier call is seen.
+  WsView v = ws_view(dev->scratch, num_reqs);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0,
+                     static_cast<hipStream_t>(stream), d_start, d_end,
+                     num_reqs, row_base, d_req_row_base, v.hdr, v.prefix,
+                     v.first_row, v.start, d_status);
+  if (hipGetLastError() != hipSuccess) return LUMEN_ERR_HIP;
+  return launch_copy(true, layout, d_cache, d_ckpt, d_block_tables, bt_cols,
+                     num_reqs, dev->scratch, 0, INT64_MAX, 0, ckpt_rows,
+                     stream, 0, d_status);
 }
 
 int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
@@ -1550,6 +1618,8 @@ const char *lumen_kv_ckpt_strerror(int code) {
       return "checkpoint row outside the checkpoint buffer, or host memory "
              "exhausted";
     case LUMEN_ERR_DUP_BLOCK: return "block named by two pages of an unpack";
+    case LUMEN_ERR_TOO_MANY:
+      return "more requests than the allocation-free call's scratch holds";
     default: return "unknown status";
   }
 }

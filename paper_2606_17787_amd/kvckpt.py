@@ -35,6 +35,8 @@ LUMEN_ERR_RANGE = -5
 LUMEN_ERR_BLOCK_ID = -6
 LUMEN_ERR_CAPACITY = -7
 LUMEN_ERR_DUP_BLOCK = -8
+LUMEN_ERR_TOO_MANY = -9
+LUMEN_KV_CKPT_NOALLOC_MAX_REQS = 16384  # include/lumen_kv_ckpt.h
 LUMEN_CACHE_NHD = 0
 LUMEN_CACHE_HND = 1
 
@@ -83,6 +85,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_plan": (ctypes.c_int, [p, p, i32, i64, p, p, p]),
         "lumen_kv_ckpt_pack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
         "lumen_kv_ckpt_unpack": (ctypes.c_int, [lay, p, p, i32, i32, p, p, i64, p]),
+        "lumen_kv_ckpt_pack_noalloc": (ctypes.c_int,
+                                       [lay, p, p, i32, p, p, i32, i64, p, p,
+                                        i64, p, p]),
         "lumen_kv_ckpt_status": (ctypes.c_int, [p, p]),
         "lumen_kv_ckpt_marks_bytes": (sz, [i64]),
         "lumen_kv_draft_align": (ctypes.c_int,
@@ -330,6 +335,45 @@ def lumen_kv_ckpt_pack(shape, num_blocks: int, cache: torch.Tensor,
     ckpt.numel() // row_elems)."""
     _copy("lumen_kv_ckpt_pack", shape, num_blocks, cache, block_tables,
           workspace, ckpt, stream)
+
+
+def lumen_kv_ckpt_pack_noalloc(shape, num_blocks: int, cache: torch.Tensor,
+                               block_tables: torch.Tensor,
+                               start: torch.Tensor, end: torch.Tensor,
+                               ckpt: torch.Tensor, status: torch.Tensor,
+                               row_base: int = 0,
+                               req_row_base: Optional[torch.Tensor] = None,
+                               stream: Optional[torch.cuda.Stream] = None
+                               ) -> None:
+    """Plan + pack with the library's own device scratch instead of a
+    workspace (for callers that cannot allocate).  `status` is a device
+    int32 tensor of one element that receives the call's status once the
+    stream has passed it."""
+    R = start.numel()
+    if end.numel() != R:
+        raise ValueError("start and end differ in length")
+    _check_tables(block_tables, R)
+    _check_cache(shape, num_blocks, cache, "cache")
+    if (ckpt.element_size() != _elem_bytes(shape)
+            or ckpt.numel() % _row_elems(shape)):
+        raise ValueError("checkpoint must hold whole rows of "
+                         f"{_elem_bytes(shape)}-byte elements")
+    if status.numel() != 1:
+        raise ValueError("status must be one int32 element")
+    pb = None
+    if req_row_base is not None:
+        if req_row_base.numel() != R:
+            raise ValueError("req_row_base must have one entry per request")
+        pb = _dev(req_row_base, "req_row_base", torch.int64)
+    lay = layout(shape, num_blocks)
+    _check(load_library().lumen_kv_ckpt_pack_noalloc(
+        ctypes.byref(lay), _dev(cache, "cache"),
+        _dev(block_tables, "block_tables", torch.int32),
+        block_tables.shape[1], _dev(start, "start", torch.int32),
+        _dev(end, "end", torch.int32), R, int(row_base), pb,
+        _dev(ckpt, "ckpt"), ckpt.numel() // _row_elems(shape),
+        _dev(status, "status", torch.int32), _stream_handle(stream)),
+        "lumen_kv_ckpt_pack_noalloc")
 
 
 def lumen_kv_ckpt_unpack(shape, num_blocks: int, cache: torch.Tensor,

@@ -70,7 +70,7 @@ def test_missing_library_fails_loudly(tmp_path):
 
 
 def test_strerror(lib):
-    for code in range(-8, 1):
+    for code in range(-9, 1):
         assert kv.lumen_kv_ckpt_strerror(code) not in ("", "unknown status")
     assert kv.lumen_kv_ckpt_strerror(-99) == "unknown status"
 

@@ -6,13 +6,19 @@ Llama-3-8B-shaped workload (32 layers, 8 KV heads, head_dim 128, block 16,
 bf16; 256 requests with lognormal contexts; every step checkpoints each
 request's newest 1-16 tokens):
 
-    plan(step k)  -> pack(step k)    source pool -> checkpoint region k
-    plan(step k') -> unpack(step k') checkpoint region k' -> restore pool
+    plan(step k)  -> pack(step k)    source pool -> checkpoint region k mod 20
+    plan(step k') -> unpack(step k') checkpoint region k' mod 20 -> restore pool
 
-with k' = k + 50 (mod 100), so the restore reads a region written 50 steps
-(about 28 GB of traffic) earlier, never a copy still held in the 256 MB
-Infinity Cache.  Inputs (pools, block tables, ranges) are resident in HBM
-before timing; the device error word is checked after the timed loop.
+with k' = k + 10, so the restore reads a region packed 10 steps (about
+5.7 GB of traffic) earlier, never a copy still held in the 256 MB Infinity
+Cache.  Where a buffer lands in physical memory moves the copies by up to
+15%, so the written buffers (restore pool and 20-region arena) are
+allocated --placements times (default 3) over one source pool, the timed
+steps rotate over those sets, and each set is then timed alone.  Inputs
+(pools, block tables, ranges) are resident in HBM before timing; the device
+error word is checked after the timed loop.  Per-kernel times: HIP events
+around every launch of the timed steps (every 5th once that gives 20 or
+more samples).
 
 Further legs (reported beside the headline, not part of its value):
   * tiny            the 8-request, 1.77 MB full pack and restore: launch
@@ -57,7 +63,8 @@ METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
 ALL_LEGS = ("decode", "tiny", "qwen", "restore", "tp8", "stage", "tags",
             "sched", "draft", "cpu")
-EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step
+EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step ...
+MIN_KERNEL_SAMPLES = 20  # ... or on every step while that gives fewer
 
 
 def parse():
@@ -67,6 +74,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--legs", default=",".join(ALL_LEGS),
                     help="comma list of " + ",".join(ALL_LEGS))
+    ap.add_argument("--placements", type=int, default=3,
+                    help="independently allocated (restore pool, arena) "
+                    "sets of the headline decode leg")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU oracle sample")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -154,36 +164,85 @@ def say(msg):
 
 # --------------------------------------------------------------- GPU legs
 
-def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None):
-    """Decode loop: step i packs step k = i mod S and restores step
-    k + S/2; per-kernel times from HIP events on the launch stream.
+def _event_steps(steps):
+    """Timed steps that carry per-kernel HIP events: every step when that
+    still gives under 100 samples, else every EVENT_EVERY-th (an event pair
+    costs a few microseconds of pipeline drain, which would otherwise
+    inflate every step's wall time).  Never fewer than MIN_KERNEL_SAMPLES
+    while the run has that many steps."""
+    every = 1 if steps < EVENT_EVERY * MIN_KERNEL_SAMPLES else EVENT_EVERY
+    return list(range(0, steps, every))
 
-    keep: a dict that carries the source pool, restore pool and arena from
-    one call to the next (None: allocate and free here).  Workloads of the
-    same byte sizes then run on the same physical memory, so that their
-    rates differ only by what the workloads do, not by where the buffers
-    landed."""
+
+def _kernel_stats(byts, ms):
+    """GB/s (summed bytes over summed time), mean / median / p10 / p90 us per
+    launch, of one kernel's sampled launches."""
+    byts, ms = np.asarray(byts, np.float64), np.asarray(ms, np.float64)
+    return dict(GBps=gb(byts.sum()) / (ms.sum() / 1e3),
+                us_mean=float(ms.mean() * 1e3),
+                us_median=float(np.median(ms) * 1e3),
+                us_p10_p90=[float(np.percentile(ms, q) * 1e3)
+                            for q in (10, 90)],
+                samples=int(ms.size), bytes_mean=float(byts.mean()))
+
+
+def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
+                    placements=1, regions=None, placement_steps=24):
+    """Decode loop: step i packs step k = i mod S into its checkpoint region
+    and restores step k + lag from the region packed lag steps earlier (lag =
+    half the regions), so the restore never reads a copy still held in the
+    256 MB Infinity Cache.  Per-kernel times from HIP events on the launch
+    stream.
+
+    placements: independently allocated sets of written buffers
+    (destination pool and arena), all resident at once, over one source
+    pool.  Where a buffer lands in physical memory moves the copies by up to
+    15%, so the timed steps rotate over the sets, and a pass after the timed
+    region times placement_steps steps on each set alone.
+    regions: checkpoint regions per arena (None: one per step, laid out back
+    to back); fewer regions, each sized to the largest step, keep several
+    arenas within HBM.
+    keep: a dict that carries the buffers from one call to the next (one
+    placement only; None: allocate and free here).  Workloads of the same
+    byte sizes then run on the same physical memory, so that their rates
+    differ only by what the workloads do, not by where the buffers landed."""
     dev = torch.device("cuda:0")
     sh = w.shape
     S = w.num_steps
     rows = np.array([w.step_tokens(k) for k in range(S)], np.int64)
-    row_off = np.concatenate([[0], np.cumsum(rows)])
     row_elems = sh.token_row_elems
+    rb = sh.token_row_bytes
+    if regions is None or regions >= S:
+        NR = S
+        region_row = np.concatenate([[0], np.cumsum(rows)])[:S]
+        arena_rows = int(rows.sum())
+    else:
+        if S % regions or regions % 2:
+            raise ValueError("regions must be even and divide the steps")
+        NR = regions
+        region_row = (np.arange(S) % NR) * int(rows.max())
+        arena_rows = NR * int(rows.max())
+    lag = NR // 2
+    P = placements
+    if keep is not None and P != 1:
+        raise ValueError("buffers are kept across legs for one placement")
 
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
     sizes = (sh.pool_elems(w.num_blocks), sh.pool_elems(w.dst_num_blocks),
-             int(row_off[-1]) * row_elems)
+             arena_rows * row_elems)
     if keep is not None and keep.get("sizes") == sizes:
         src, dst, arena = keep.pop("bufs")
         dst.zero_()
+        sets = [(dst, arena)]
     else:
         if keep is not None:
             keep.clear()
             torch.cuda.empty_cache()
         src = torch.empty(sizes[0], dtype=torch.bfloat16, device=dev)
-        dst = torch.zeros(sizes[1], dtype=torch.bfloat16, device=dev)
-        arena = torch.empty(sizes[2], dtype=torch.bfloat16, device=dev)
+        sets = [(torch.zeros(sizes[1], dtype=torch.bfloat16, device=dev),
+                 torch.empty(sizes[2], dtype=torch.bfloat16, device=dev))
+                for _ in range(P)]
     src.normal_(generator=g)
     bt = torch.from_numpy(w.block_tables).to(dev)
     bt_dst = torch.from_numpy(w.dst_block_tables).to(dev)
@@ -192,35 +251,40 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None):
     ws_a = kv.new_workspace(w.num_reqs, dev)
     ws_b = kv.new_workspace(w.num_reqs, dev)
 
-    # Fill every checkpoint region once (also the first correctness gate).
-    for k in range(S):
-        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, int(row_off[k]))
-        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
+    # Fill every checkpoint region of every arena once (also the first
+    # correctness gate).
+    for _, arena in sets:
+        for k in range(S):
+            kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, int(region_row[k]))
+            kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
     st = kv.lumen_kv_ckpt_status(ws_a)
     if st != 0:
         raise RuntimeError(f"pack reported {kv.lumen_kv_ckpt_strerror(st)}")
 
-    # Per-kernel times come from HIP events on every EVENT_EVERY-th step of
-    # the timed region: an event pair costs a few microseconds of pipeline
-    # drain, which would otherwise inflate every step's wall time.
-    sampled = list(range(0, steps, EVENT_EVERY))
-    ev = {i: [TimingEvent() for _ in range(4)]
-          for i in sampled}
-
-    def step(i, events=None):
+    def step(i, events=None, p=None):
         k = i % S
-        k2 = (k + S // 2) % S
-        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, int(row_off[k]))
+        k2 = (k + lag) % S
+        dst, arena = sets[i % P if p is None else p]
+        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, int(region_row[k]))
         if events: events[0].record()
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
         if events: events[1].record()
-        kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, int(row_off[k2]))
+        kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, int(region_row[k2]))
         if events: events[2].record()
         kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt_dst, ws_b,
                                 arena)
         if events: events[3].record()
         return k, k2
 
+    def sampled_stats(done, ev, idx):
+        pk = _kernel_stats([2 * rows[done[i][0]] * rb for i in idx],
+                           [ev[i][0].elapsed_time(ev[i][1]) for i in idx])
+        up = _kernel_stats([2 * rows[done[i][1]] * rb for i in idx],
+                           [ev[i][2].elapsed_time(ev[i][3]) for i in idx])
+        return pk, up
+
+    sampled = _event_steps(steps)
+    ev = {i: [TimingEvent() for _ in range(4)] for i in sampled}
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
@@ -231,47 +295,68 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None):
     st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
     if st != 0:
         raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
-
-    rb = sh.token_row_bytes
-    pack_b = np.array([2 * rows[done[i][0]] * rb for i in sampled], np.float64)
-    unpack_b = np.array([2 * rows[done[i][1]] * rb for i in sampled],
-                        np.float64)
+    pack, unpack = sampled_stats(done, ev, sampled)
     step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in done)
-    pack_ms = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in sampled])
-    unpack_ms = np.array([ev[i][2].elapsed_time(ev[i][3]) for i in sampled])
     wall_ms = (t1 - t0) * 1e3
 
+    # Each placement alone, after the timed region.
+    per_placement = []
+    if P > 1:
+        for p in range(P):
+            evp = {i: [TimingEvent() for _ in range(4)]
+                   for i in range(placement_steps)}
+            for i in range(4):
+                step(i, p=p)
+            dn = [step(i, evp[i], p=p) for i in range(placement_steps)]
+            torch.cuda.synchronize()
+            pk, up = sampled_stats(dn, evp, range(placement_steps))
+            per_placement.append(dict(
+                pack_GBps=pk["GBps"], unpack_GBps=up["GBps"],
+                pack_us_median=pk["us_median"],
+                unpack_us_median=up["us_median"],
+                pack_us_p10_p90=pk["us_p10_p90"],
+                unpack_us_p10_p90=up["us_p10_p90"], samples=pk["samples"]))
+        st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
+        if st != 0:
+            raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
+
     # Round trip as a self-check (no oracle here): re-pack the restored
-    # tokens of one step from the restore pool and compare with its region.
+    # tokens of one step from the restore pool and compare with the region
+    # the unpack read.
+    i_last = warmup + steps - 1
     k = done[-1][1]
+    dst, arena = sets[i_last % P]
     kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_b, 0)
     back = torch.empty(int(rows[k]) * row_elems, dtype=torch.bfloat16,
                        device=dev)
     kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, dst, bt_dst, ws_b, back)
-    region = arena[int(row_off[k]) * row_elems:int(row_off[k + 1]) * row_elems]
+    r0 = int(region_row[k])
+    region = arena[r0 * row_elems:(r0 + int(rows[k])) * row_elems]
     roundtrip = bool(torch.equal(back.view(torch.int16),
                                  region.view(torch.int16)))
     assert kv.lumen_kv_ckpt_status(ws_b) == 0
 
     # The per-request row mode: one checkpoint per request (Sec. 4.2), the
-    # increments of request r appending to its own region of the same
+    # increments of request r appending to its own region of the first
     # arena, so a step's rows land in up to R places instead of one run.
-    inc = w.ends[-1].astype(np.int64) - w.starts[0].astype(np.int64)
-    assert int(inc.sum()) == int(row_off[-1])
+    # Steps 0 .. NR-1 fill the arena exactly.
+    dst, arena = sets[0]
+    inc = w.ends[NR - 1].astype(np.int64) - w.starts[0].astype(np.int64)
+    assert int(inc.sum()) == int(rows[:NR].sum()) <= arena_rows
     region0 = np.concatenate([[0], np.cumsum(inc)[:-1]])
     rrb_h = region0 - w.starts[0].astype(np.int64)  # row of token t: rrb + t
     rrb = torch.from_numpy(rrb_h).to(dev)
-    for k in range(S):
+    for k in range(NR):
         kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
     assert kv.lumen_kv_ckpt_status(ws_a) == 0
-    pr_steps = max(steps // 2, EVENT_EVERY)
-    pr_ev = {i: [TimingEvent() for _ in range(4)]
-             for i in range(0, pr_steps, EVENT_EVERY)}
+    pr_steps = max(steps // 2, MIN_KERNEL_SAMPLES)
+    pr_sampled = _event_steps(pr_steps)
+    pr_ev = {i: [TimingEvent() for _ in range(4)] for i in pr_sampled}
 
     def step_pr(i, events=None):
-        k = i % S
-        k2 = (k + S // 2) % S
+        k = i % NR
+        k2 = (k + lag) % NR
         kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
         if events: events[0].record()
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
@@ -292,11 +377,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None):
     t3 = time.perf_counter()
     assert min(kv.lumen_kv_ckpt_status(ws_a),
                kv.lumen_kv_ckpt_status(ws_b)) == 0
-    pr_s = sorted(pr_ev)
-    pr_pack_b = sum(2.0 * rows[pr_done[i][0]] * rb for i in pr_s)
-    pr_unpack_b = sum(2.0 * rows[pr_done[i][1]] * rb for i in pr_s)
-    pr_pack_ms = sum(pr_ev[i][0].elapsed_time(pr_ev[i][1]) for i in pr_s)
-    pr_unpack_ms = sum(pr_ev[i][2].elapsed_time(pr_ev[i][3]) for i in pr_s)
+    pr_pack, pr_unpack = sampled_stats(pr_done, pr_ev, pr_sampled)
     pr_step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in pr_done)
     # self-check: one step's rows, gathered from the request regions, equal
     # the same step packed contiguously
@@ -316,38 +397,44 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None):
     per_request_mode = dict(
         steps=pr_steps, ms_per_step=(t3 - t2) * 1e3 / pr_steps,
         step_GBps=gb(pr_step_b) / (t3 - t2),
-        pack_GBps=gb(pr_pack_b) / (pr_pack_ms / 1e3),
-        unpack_GBps=gb(pr_unpack_b) / (pr_unpack_ms / 1e3),
-        check_ok=pr_ok)
+        pack_GBps=pr_pack["GBps"], unpack_GBps=pr_unpack["GBps"],
+        pack_us_median=pr_pack["us_median"],
+        unpack_us_median=pr_unpack["us_median"],
+        samples=pr_pack["samples"], check_ok=pr_ok)
     if keep is not None:
-        keep["sizes"], keep["bufs"] = sizes, (src, dst, arena)
-    del src, dst, arena, back, gathered
+        keep["sizes"], keep["bufs"] = sizes, (src, sets[0][0], sets[0][1])
+    del src, sets, dst, arena, back, gathered
     if keep is None:
         torch.cuda.empty_cache()
 
-    pack_GBps = gb(pack_b.sum()) / (pack_ms.sum() / 1e3)
-    unpack_GBps = gb(unpack_b.sum()) / (unpack_ms.sum() / 1e3)
-    return dict(
-        workload=w.name, steps=steps, warmup=warmup,
-        wall_ms=wall_ms, ms_per_step=wall_ms / steps,
+    out = dict(
+        workload=w.name, fingerprint=w.fingerprint(), steps=steps,
+        warmup=warmup, wall_ms=wall_ms, ms_per_step=wall_ms / steps,
         step_GBps=gb(step_b) / (wall_ms / 1e3), sampled_steps=len(sampled),
-        pack_GBps=pack_GBps, unpack_GBps=unpack_GBps,
-        pack_pct_peak=100 * pack_GBps / HBM_PEAK_GBPS,
-        unpack_pct_peak=100 * unpack_GBps / HBM_PEAK_GBPS,
-        pack_us_mean=float(pack_ms.mean() * 1e3),
-        unpack_us_mean=float(unpack_ms.mean() * 1e3),
-        pack_us_median=float(np.median(pack_ms) * 1e3),
-        unpack_us_median=float(np.median(unpack_ms) * 1e3),
-        pack_us_p10_p90=[float(np.percentile(pack_ms, q) * 1e3)
-                         for q in (10, 90)],
-        unpack_us_p10_p90=[float(np.percentile(unpack_ms, q) * 1e3)
-                           for q in (10, 90)],
-        pack_bytes_mean=float(pack_b.mean()),
-        unpack_bytes_mean=float(unpack_b.mean()),
+        placements=P, regions=NR,
+        pack_GBps=pack["GBps"], unpack_GBps=unpack["GBps"],
+        pack_pct_peak=100 * pack["GBps"] / HBM_PEAK_GBPS,
+        unpack_pct_peak=100 * unpack["GBps"] / HBM_PEAK_GBPS,
+        pack_us_mean=pack["us_mean"], unpack_us_mean=unpack["us_mean"],
+        pack_us_median=pack["us_median"],
+        unpack_us_median=unpack["us_median"],
+        pack_us_p10_p90=pack["us_p10_p90"],
+        unpack_us_p10_p90=unpack["us_p10_p90"],
+        pack_bytes_mean=pack["bytes_mean"],
+        unpack_bytes_mean=unpack["bytes_mean"],
         tokens_per_step_mean=float(rows.mean()),
         roundtrip_ok=roundtrip,
         per_request_mode=per_request_mode,
     )
+    if per_placement:
+        out["per_placement"] = per_placement
+        for op in ("pack", "unpack"):
+            v = sorted(x[f"{op}_GBps"] for x in per_placement)
+            out[f"{op}_placement_worst_GBps"] = v[0]
+            out[f"{op}_placement_median_GBps"] = float(np.median(v))
+            out[f"{op}_placement_worst_pct_peak"] = \
+                100 * v[0] / HBM_PEAK_GBPS
+    return out
 
 
 def restore_leg(torch, kv, W):
@@ -1264,6 +1351,23 @@ def rounded(d):
     return {k: r(v) for k, v in d.items()}
 
 
+def environment(torch):
+    """GPU, runtime and library versions of the run."""
+    props = torch.cuda.get_device_properties(0)
+    rocm = None
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            rocm = f.read().strip()
+    except OSError:
+        pass
+    return {"gpu": torch.cuda.get_device_name(0),
+            "arch": getattr(props, "gcnArchName", None),
+            "cus": props.multi_processor_count,
+            "hbm_GiB": round(props.total_memory / 2**30, 1),
+            "rocm": rocm, "hip": torch.version.hip,
+            "torch": torch.__version__, "numpy": np.__version__}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -1283,7 +1387,8 @@ def main():
 
     say("[bench] decode leg (llama3-8b-decode)")
     w = W.c2_llama8b()
-    dec = incremental_leg(torch, kv, w, args.steps, args.warmup, seed=2)
+    dec = incremental_leg(torch, kv, w, args.steps, args.warmup, seed=2,
+                          placements=args.placements, regions=20)
     dominant = ("pack" if dec["pack_us_mean"] >= dec["unpack_us_mean"]
                 else "unpack")
     achieved = dec[f"{dominant}_GBps"]
@@ -1299,14 +1404,28 @@ def main():
                    "block_size": w.shape.block_size,
                    "cache_layout": w.shape.order, "requests": w.num_reqs,
                    "tokens_per_step_mean": dec["tokens_per_step_mean"],
-                   "step": "plan+pack of step k, plan+unpack of step k+50",
+                   "step": "plan+pack of step k, plan+unpack of step k+10 "
+                           "(20 checkpoint regions per arena)",
+                   "placements": dec["placements"],
+                   "fingerprint": dec["fingerprint"],
                    "parallelism": "none (1 GPU)"},
+        "env": environment(torch),
         "pack_GBps": round(dec["pack_GBps"], 1),
         "unpack_GBps": round(dec["unpack_GBps"], 1),
         "pack_pct_peak": round(dec["pack_pct_peak"], 2),
         "unpack_pct_peak": round(dec["unpack_pct_peak"], 2),
         "pack_us_mean": round(dec["pack_us_mean"], 2),
         "unpack_us_mean": round(dec["unpack_us_mean"], 2),
+        "pack_us_median": round(dec["pack_us_median"], 2),
+        "unpack_us_median": round(dec["unpack_us_median"], 2),
+        "pack_us_p10_p90": [round(x, 2) for x in dec["pack_us_p10_p90"]],
+        "unpack_us_p10_p90": [round(x, 2) for x in dec["unpack_us_p10_p90"]],
+        "kernel_samples": dec["sampled_steps"],
+        "placement": rounded({k: dec[k] for k in (
+            "pack_placement_worst_GBps", "pack_placement_median_GBps",
+            "pack_placement_worst_pct_peak", "unpack_placement_worst_GBps",
+            "unpack_placement_median_GBps", "unpack_placement_worst_pct_peak",
+            "per_placement") if k in dec}),
         "roundtrip_ok": dec["roundtrip_ok"],
         "per_request_mode": rounded(dec["per_request_mode"]),
         "roofline": {"bound": "hbm",

@@ -401,6 +401,21 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         pack_us_median=pr_pack["us_median"],
         unpack_us_median=pr_unpack["us_median"],
         samples=pr_pack["samples"], check_ok=pr_ok)
+    # The write rate of each restore pool itself: a plain sequential fill
+    # (torch's), the ceiling the scattered restore writes run against.  The
+    # same kernel and data run up to 20% apart between pools, by where the
+    # pool landed in physical memory.
+    if per_placement:
+        for p, (d, _) in enumerate(sets):
+            a, b = TimingEvent(), TimingEvent()
+            d.zero_()
+            a.record()
+            for _ in range(3):
+                d.zero_()
+            b.record()
+            b.synchronize()
+            per_placement[p]["restore_pool_fill_GBps"] = \
+                gb(3.0 * d.numel() * d.element_size()) / (a.elapsed_time(b) / 1e3)
     if keep is not None:
         keep["sizes"], keep["bufs"] = sizes, (src, sets[0][0], sets[0][1])
     del src, sets, dst, arena, back, gathered

@@ -184,6 +184,10 @@ def check_all_rows(shape, pool, nb, bt, s, e, ck, row_base, what,
                 raise AssertionError(
                     f"{what}: rows {int(prow[i])}..{int(prow[i]) + rows}: "
                     f"first differing elements {bad}")
+            # one line per chunk, so that no phase of the host-side oracle
+            # checks runs silently for long
+            say(f"[fullsize] {what}: rows {int(prow[i])}..{int(prow[i]) + rows}"
+                " equal the oracle")
             i = j
 
 

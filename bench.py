@@ -16,9 +16,10 @@ Cache.  Where a buffer lands in physical memory moves the copies by up to
 allocated --placements times (default 3) over one source pool, the timed
 steps rotate over those sets, and each set is then timed alone.  Inputs
 (pools, block tables, ranges) are resident in HBM before timing; the device
-error word is checked after the timed loop.  Per-kernel times: HIP events
-around every launch of the timed steps (every 5th once that gives 20 or
-more samples).
+error word is checked after the timed loop.  The value is the timed pass:
+exactly --steps steps with nothing else on the stream.  Per-kernel times
+come from an event pass right after it: the same steps again (at least 20),
+every launch bracketed by HIP events on its stream.
 
 Further legs (reported beside the headline, not part of its value):
   * tiny            the 8-request, 1.77 MB full pack and restore: launch
@@ -63,8 +64,7 @@ METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
 ALL_LEGS = ("decode", "tiny", "qwen", "restore", "tp8", "stage", "tags",
             "sched", "draft", "cpu")
-EVENT_EVERY = 5  # per-kernel HIP events on every 5th timed step ...
-MIN_KERNEL_SAMPLES = 20  # ... or on every step while that gives fewer
+MIN_KERNEL_SAMPLES = 20  # fewest timed launches of a per-kernel figure
 
 
 def parse():
@@ -165,13 +165,9 @@ def say(msg):
 # --------------------------------------------------------------- GPU legs
 
 def _event_steps(steps):
-    """Timed steps that carry per-kernel HIP events: every step when that
-    still gives under 100 samples, else every EVENT_EVERY-th (an event pair
-    costs a few microseconds of pipeline drain, which would otherwise
-    inflate every step's wall time).  Never fewer than MIN_KERNEL_SAMPLES
-    while the run has that many steps."""
-    every = 1 if steps < EVENT_EVERY * MIN_KERNEL_SAMPLES else EVENT_EVERY
-    return list(range(0, steps, every))
+    """Steps of the event pass: as many as the timed pass, and never fewer
+    than MIN_KERNEL_SAMPLES."""
+    return list(range(max(steps, MIN_KERNEL_SAMPLES)))
 
 
 def _kernel_stats(byts, ms):
@@ -283,28 +279,41 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                            [ev[i][2].elapsed_time(ev[i][3]) for i in idx])
         return pk, up
 
-    sampled = _event_steps(steps)
-    ev = {i: [TimingEvent() for _ in range(4)] for i in sampled}
+    def events(n):
+        return {i: [TimingEvent() for _ in range(4)] for i in n}
+
+    # The timed pass (the value): exactly `steps` steps with nothing but
+    # the copies and their plans on the stream.
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    done = [step(warmup + i, ev.get(i)) for i in range(steps)]
+    done = [step(warmup + i) for i in range(steps)]
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
     if st != 0:
         raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
-    pack, unpack = sampled_stats(done, ev, sampled)
     step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in done)
     wall_ms = (t1 - t0) * 1e3
+    # The event pass (the per-kernel figures): the same steps again, from
+    # the same schedule position, each launch bracketed by HIP events on its
+    # stream.  The events cost a few us per step, so they stay out of the
+    # timed pass.
+    sampled = _event_steps(steps)
+    ev = events(sampled)
+    done_ev = [step(warmup + i, ev[i]) for i in sampled]
+    torch.cuda.synchronize()
+    st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
+    if st != 0:
+        raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
+    pack, unpack = sampled_stats(done_ev, ev, sampled)
 
     # Each placement alone, after the timed region.
     per_placement = []
     if P > 1:
         for p in range(P):
-            evp = {i: [TimingEvent() for _ in range(4)]
-                   for i in range(placement_steps)}
+            evp = events(range(placement_steps))
             for i in range(4):
                 step(i, p=p)
             dn = [step(i, evp[i], p=p) for i in range(placement_steps)]
@@ -351,8 +360,6 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
     assert kv.lumen_kv_ckpt_status(ws_a) == 0
     pr_steps = max(steps // 2, MIN_KERNEL_SAMPLES)
-    pr_sampled = _event_steps(pr_steps)
-    pr_ev = {i: [TimingEvent() for _ in range(4)] for i in pr_sampled}
 
     def step_pr(i, events=None):
         k = i % NR
@@ -372,12 +379,16 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         step_pr(i)
     torch.cuda.synchronize()
     t2 = time.perf_counter()
-    pr_done = [step_pr(warmup + i, pr_ev.get(i)) for i in range(pr_steps)]
+    pr_done = [step_pr(warmup + i) for i in range(pr_steps)]
     torch.cuda.synchronize()
     t3 = time.perf_counter()
+    pr_sampled = _event_steps(pr_steps)
+    pr_ev = events(pr_sampled)
+    pr_done_ev = [step_pr(warmup + i, pr_ev[i]) for i in pr_sampled]
+    torch.cuda.synchronize()
     assert min(kv.lumen_kv_ckpt_status(ws_a),
                kv.lumen_kv_ckpt_status(ws_b)) == 0
-    pr_pack, pr_unpack = sampled_stats(pr_done, pr_ev, pr_sampled)
+    pr_pack, pr_unpack = sampled_stats(pr_done_ev, pr_ev, pr_sampled)
     pr_step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in pr_done)
     # self-check: one step's rows, gathered from the request regions, equal
     # the same step packed contiguously
@@ -401,21 +412,6 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         pack_us_median=pr_pack["us_median"],
         unpack_us_median=pr_unpack["us_median"],
         samples=pr_pack["samples"], check_ok=pr_ok)
-    # The write rate of each restore pool itself: a plain sequential fill
-    # (torch's), the ceiling the scattered restore writes run against.  The
-    # same kernel and data run up to 20% apart between pools, by where the
-    # pool landed in physical memory.
-    if per_placement:
-        for p, (d, _) in enumerate(sets):
-            a, b = TimingEvent(), TimingEvent()
-            d.zero_()
-            a.record()
-            for _ in range(3):
-                d.zero_()
-            b.record()
-            b.synchronize()
-            per_placement[p]["restore_pool_fill_GBps"] = \
-                gb(3.0 * d.numel() * d.element_size()) / (a.elapsed_time(b) / 1e3)
     if keep is not None:
         keep["sizes"], keep["bufs"] = sizes, (src, sets[0][0], sets[0][1])
     del src, sets, dst, arena, back, gathered

@@ -147,6 +147,13 @@ def _stream_handle(stream: Optional[torch.cuda.Stream]):
         torch.cuda.current_device()))
 
 
+def _required_stream(stream) -> ctypes.c_void_p:
+    if not isinstance(stream, torch.cuda.Stream):
+        raise ValueError("the staging pipelines need explicit streams "
+                         "(torch.cuda.Stream); see their docstrings")
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
 def _dev(t: torch.Tensor, what: str, dtype=None) -> ctypes.c_void_p:
     d = t.get_device()
     if d < 0:
@@ -528,11 +535,14 @@ def lumen_kv_ckpt_pack_to_host(shape, num_blocks: int, cache: torch.Tensor,
                                block_tables: torch.Tensor,
                                workspace: torch.Tensor, total_rows: int,
                                staging: torch.Tensor, slots: int,
-                               host: torch.Tensor,
-                               pack_stream: Optional[torch.cuda.Stream] = None,
-                               copy_stream: Optional[torch.cuda.Stream] = None):
+                               host: torch.Tensor, *,
+                               pack_stream: torch.cuda.Stream,
+                               copy_stream: torch.cuda.Stream):
     """Pack the planned rows through a device staging ring of `slots` equal
-    slots (`staging` is split evenly) into host tensor `host` (pinned)."""
+    slots (`staging` is split evenly) into host tensor `host` (pinned).
+    Both streams are required: for the checkpoint to overlap serving they
+    must differ from the serving stream (passing the serving stream, e.g.
+    torch.cuda.current_stream(), runs the pipeline serially on it)."""
     R, slot_rows = _pipeline_args(shape, num_blocks, cache, block_tables,
                                   workspace, total_rows, staging, slots, host)
     lay = layout(shape, num_blocks)
@@ -541,8 +551,8 @@ def lumen_kv_ckpt_pack_to_host(shape, num_blocks: int, cache: torch.Tensor,
         _dev(block_tables, "block_tables", torch.int32),
         block_tables.shape[1], R, _dev(workspace, "workspace"),
         int(total_rows), _dev(staging, "staging"), slot_rows, int(slots),
-        ctypes.c_void_p(host.data_ptr()), _stream_handle(pack_stream),
-        _stream_handle(copy_stream)), "lumen_kv_ckpt_pack_to_host")
+        ctypes.c_void_p(host.data_ptr()), _required_stream(pack_stream),
+        _required_stream(copy_stream)), "lumen_kv_ckpt_pack_to_host")
 
 
 def lumen_kv_ckpt_unpack_from_host(shape, num_blocks: int,
@@ -550,11 +560,12 @@ def lumen_kv_ckpt_unpack_from_host(shape, num_blocks: int,
                                    block_tables: torch.Tensor,
                                    workspace: torch.Tensor, total_rows: int,
                                    host: torch.Tensor, staging: torch.Tensor,
-                                   slots: int,
-                                   copy_stream: Optional[torch.cuda.Stream] = None,
-                                   unpack_stream: Optional[torch.cuda.Stream] = None):
+                                   slots: int, *,
+                                   copy_stream: torch.cuda.Stream,
+                                   unpack_stream: torch.cuda.Stream):
     """Restore the planned rows from host tensor `host` through the staging
-    ring into `cache`."""
+    ring into `cache`.  Both streams are required, as for
+    lumen_kv_ckpt_pack_to_host."""
     R, slot_rows = _pipeline_args(shape, num_blocks, cache, block_tables,
                                   workspace, total_rows, staging, slots, host)
     lay = layout(shape, num_blocks)
@@ -564,7 +575,7 @@ def lumen_kv_ckpt_unpack_from_host(shape, num_blocks: int,
         block_tables.shape[1], R, _dev(workspace, "workspace"),
         int(total_rows), ctypes.c_void_p(host.data_ptr()),
         _dev(staging, "staging"), slot_rows, int(slots),
-        _stream_handle(copy_stream), _stream_handle(unpack_stream)),
+        _required_stream(copy_stream), _required_stream(unpack_stream)),
         "lumen_kv_ckpt_unpack_from_host")
 
 

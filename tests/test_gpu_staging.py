@@ -365,18 +365,27 @@ def test_pipeline_rejects_misused_buffers():
     small_host = torch.zeros(total * rb - 16, dtype=torch.uint8,
                              pin_memory=True)
     staging = torch.empty(2 * 4 * rb, dtype=torch.uint8, device=dev())
+    ps, cs = torch.cuda.Stream(), torch.cuda.Stream()
     with pytest.raises(ValueError):   # host copy smaller than the rows
         kv.lumen_kv_ckpt_pack_to_host(shape, nb, h2d(src), h2d(bt), ws,
-                                      total, staging, 2, small_host)
+                                      total, staging, 2, small_host,
+                                      pack_stream=ps, copy_stream=cs)
     with pytest.raises(ValueError):   # staging not whole rows per slot
         kv.lumen_kv_ckpt_pack_to_host(
             shape, nb, h2d(src), h2d(bt), ws, total,
             torch.empty(2 * 4 * rb + 16, dtype=torch.uint8, device=dev()),
-            2, torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True))
+            2, torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True),
+            pack_stream=ps, copy_stream=cs)
     with pytest.raises(ValueError):   # host tensor on the device
         kv.lumen_kv_ckpt_pack_to_host(
             shape, nb, h2d(src), h2d(bt), ws, total, staging, 2,
-            torch.zeros(total * rb, dtype=torch.uint8, device=dev()))
+            torch.zeros(total * rb, dtype=torch.uint8, device=dev()),
+            pack_stream=ps, copy_stream=cs)
+    with pytest.raises(ValueError):   # a stream left out
+        kv.lumen_kv_ckpt_pack_to_host(
+            shape, nb, h2d(src), h2d(bt), ws, total, staging, 2,
+            torch.zeros(total * rb, dtype=torch.uint8, pin_memory=True),
+            pack_stream=ps, copy_stream=None)
 
 
 def test_back_to_back_pipelines_share_one_ring():

@@ -1,6 +1,7 @@
 """Host-side logic of bench.py that needs no GPU: the hash that decides
 whether the committed HBM byte counters still describe the device code, and
-the refusal of more than one GPU."""
+the refusal of more than one GPU, the event pass's sample count and the
+per-kernel statistics."""
 import json
 import os
 import subprocess
@@ -55,3 +56,24 @@ def test_more_than_one_gpu_is_refused():
                        timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_event_pass_has_enough_samples():
+    """The per-kernel figures rest on at least MIN_KERNEL_SAMPLES launches
+    however few steps are timed, and on every timed step's worth when more
+    are."""
+    for steps in (1, 5, 19, 20, 37, 200):
+        n = len(bench._event_steps(steps))
+        assert n == max(steps, bench.MIN_KERNEL_SAMPLES)
+    assert bench.MIN_KERNEL_SAMPLES >= 20
+
+
+def test_kernel_stats_sum_bytes_over_sum_time():
+    """GB/s is total bytes over total time (not a mean of per-launch
+    rates); mean, median and the p10/p90 pair are in microseconds."""
+    st = bench._kernel_stats([1e9, 3e9], [1.0, 2.0])  # bytes, ms
+    assert abs(st["GBps"] - 4e9 / 3e-3 / 1e9) < 1e-6
+    assert st["us_mean"] == 1500.0 and st["us_median"] == 1500.0
+    assert st["samples"] == 2 and st["bytes_mean"] == 2e9
+    lo, hi = st["us_p10_p90"]
+    assert 1000.0 < lo < hi < 2000.0

@@ -6,12 +6,15 @@ Llama-3-8B-shaped workload (32 layers, 8 KV heads, head_dim 128, block 16,
 bf16; 256 requests with lognormal contexts; every step checkpoints each
 request's newest 1-16 tokens):
 
-    plan(step k)  -> pack(step k)    source pool -> checkpoint region k mod 20
-    plan(step k') -> unpack(step k') checkpoint region k' mod 20 -> restore pool
+    pack(step k)    source pool -> checkpoint region k mod 20
+    unpack(step k') checkpoint region k' mod 20 -> restore pool
 
 with k' = k + 10, so the restore reads a region packed 10 steps (about
 5.7 GB of traffic) earlier, never a copy still held in the 256 MB Infinity
-Cache.  Where a buffer lands in physical memory moves the copies by up to
+Cache.  Each copy is one launch that plans its rows from the token ranges
+itself (lumen_kv_ckpt_pack_ranges / _unpack_ranges); the same steps issued
+as plan + copy (a plan kernel into a workspace before each copy) are timed
+right after on the same buffers and reported as other_path.  Where a buffer lands in physical memory moves the copies by up to
 15%, so the written buffers (restore pool and 20-region arena) are
 allocated --placements times (default 3) over one source pool, the timed
 steps rotate over those sets, and each set is then timed alone.  Inputs
@@ -183,7 +186,8 @@ def _kernel_stats(byts, ms):
 
 
 def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
-                    placements=1, regions=None, placement_steps=24):
+                    placements=1, regions=None, placement_steps=24,
+                    path="plan", compare=None):
     """Decode loop: step i packs step k = i mod S into its checkpoint region
     and restores step k + lag from the region packed lag steps earlier (lag =
     half the regions), so the restore never reads a copy still held in the
@@ -201,7 +205,11 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     keep: a dict that carries the buffers from one call to the next (one
     placement only; None: allocate and free here).  Workloads of the same
     byte sizes then run on the same physical memory, so that their rates
-    differ only by what the workloads do, not by where the buffers landed."""
+    differ only by what the workloads do, not by where the buffers landed.
+    path: how a step's copies are issued: "plan" (a plan kernel into a
+    workspace before each copy) or "ranges" (each copy one launch that
+    plans from the ranges itself).  compare: the other path, timed the
+    same way right after on the same buffers (reported as other_path)."""
     dev = torch.device("cuda:0")
     sh = w.shape
     S = w.num_steps
@@ -257,19 +265,46 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     if st != 0:
         raise RuntimeError(f"pack reported {kv.lumen_kv_ckpt_strerror(st)}")
 
-    def step(i, events=None, p=None):
-        k = i % S
-        k2 = (k + lag) % S
-        dst, arena = sets[i % P if p is None else p]
-        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, int(region_row[k]))
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def copies(how, k, k2, dst, arena, events, rrb=None):
+        """Pack of step k and unpack of step k2, issued the `how` way."""
+        b1 = 0 if rrb is not None else int(region_row[k])
+        b2 = 0 if rrb is not None else int(region_row[k2])
+        if how == "ranges":
+            if events: events[0].record()
+            kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, starts[k],
+                                         ends[k], arena, status, b1, rrb)
+            if events:
+                events[1].record()
+                events[2].record()
+            kv.lumen_kv_ckpt_unpack_ranges(sh, w.dst_num_blocks, dst, bt_dst,
+                                           starts[k2], ends[k2], arena,
+                                           status, b2, rrb)
+            if events: events[3].record()
+            return
+        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, b1, rrb)
         if events: events[0].record()
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
         if events: events[1].record()
-        kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, int(region_row[k2]))
+        kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, b2, rrb)
         if events: events[2].record()
         kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt_dst, ws_b,
                                 arena)
         if events: events[3].record()
+
+    def check_status():
+        st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b),
+                 int(status.item()))
+        status.zero_()
+        if st != 0:
+            raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
+
+    def step(i, events=None, p=None, how=path):
+        k = i % S
+        k2 = (k + lag) % S
+        dst, arena = sets[i % P if p is None else p]
+        copies(how, k, k2, dst, arena, events)
         return k, k2
 
     def sampled_stats(done, ev, idx):
@@ -291,9 +326,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     done = [step(warmup + i) for i in range(steps)]
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
-    if st != 0:
-        raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
+    check_status()
     step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in done)
     wall_ms = (t1 - t0) * 1e3
     # The event pass (the per-kernel figures): the same steps again, from
@@ -304,10 +337,32 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     ev = events(sampled)
     done_ev = [step(warmup + i, ev[i]) for i in sampled]
     torch.cuda.synchronize()
-    st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
-    if st != 0:
-        raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
+    check_status()
     pack, unpack = sampled_stats(done_ev, ev, sampled)
+
+    # The other path, timed the same way on the same buffers.
+    other = None
+    if compare is not None:
+        for i in range(warmup):
+            step(i, how=compare)
+        torch.cuda.synchronize()
+        t4 = time.perf_counter()
+        done_o = [step(warmup + i, how=compare) for i in range(steps)]
+        torch.cuda.synchronize()
+        t5 = time.perf_counter()
+        check_status()
+        ev_o = events(sampled)
+        done_oev = [step(warmup + i, ev_o[i], how=compare) for i in sampled]
+        torch.cuda.synchronize()
+        check_status()
+        pk_o, up_o = sampled_stats(done_oev, ev_o, sampled)
+        other = dict(
+            path=compare, ms_per_step=(t5 - t4) * 1e3 / steps,
+            step_GBps=gb(sum(2.0 * (rows[k] + rows[k2]) * rb
+                             for k, k2 in done_o)) / (t5 - t4),
+            pack_GBps=pk_o["GBps"], unpack_GBps=up_o["GBps"],
+            pack_us_median=pk_o["us_median"],
+            unpack_us_median=up_o["us_median"])
 
     # Each placement alone, after the timed region.
     per_placement = []
@@ -318,6 +373,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                 step(i, p=p)
             dn = [step(i, evp[i], p=p) for i in range(placement_steps)]
             torch.cuda.synchronize()
+            check_status()
             pk, up = sampled_stats(dn, evp, range(placement_steps))
             per_placement.append(dict(
                 pack_GBps=pk["GBps"], unpack_GBps=up["GBps"],
@@ -325,9 +381,6 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                 unpack_us_median=up["us_median"],
                 pack_us_p10_p90=pk["us_p10_p90"],
                 unpack_us_p10_p90=up["us_p10_p90"], samples=pk["samples"]))
-        st = min(kv.lumen_kv_ckpt_status(ws_a), kv.lumen_kv_ckpt_status(ws_b))
-        if st != 0:
-            raise RuntimeError(f"device error {kv.lumen_kv_ckpt_strerror(st)}")
 
     # Round trip as a self-check (no oracle here): re-pack the restored
     # tokens of one step from the restore pool and compare with the region
@@ -364,15 +417,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     def step_pr(i, events=None):
         k = i % NR
         k2 = (k + lag) % NR
-        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
-        if events: events[0].record()
-        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
-        if events: events[1].record()
-        kv.lumen_kv_ckpt_plan(starts[k2], ends[k2], ws_b, 0, rrb)
-        if events: events[2].record()
-        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt_dst, ws_b,
-                                arena)
-        if events: events[3].record()
+        copies(path, k, k2, dst, arena, events, rrb)
         return k, k2
 
     for i in range(warmup):
@@ -386,8 +431,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     pr_ev = events(pr_sampled)
     pr_done_ev = [step_pr(warmup + i, pr_ev[i]) for i in pr_sampled]
     torch.cuda.synchronize()
-    assert min(kv.lumen_kv_ckpt_status(ws_a),
-               kv.lumen_kv_ckpt_status(ws_b)) == 0
+    check_status()
     pr_pack, pr_unpack = sampled_stats(pr_done_ev, pr_ev, pr_sampled)
     pr_step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in pr_done)
     # self-check: one step's rows, gathered from the request regions, equal
@@ -419,7 +463,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         torch.cuda.empty_cache()
 
     out = dict(
-        workload=w.name, fingerprint=w.fingerprint(), steps=steps,
+        workload=w.name, fingerprint=w.fingerprint(), path=path, steps=steps,
         warmup=warmup, wall_ms=wall_ms, ms_per_step=wall_ms / steps,
         step_GBps=gb(step_b) / (wall_ms / 1e3), sampled_steps=len(sampled),
         placements=P, regions=NR,
@@ -437,6 +481,8 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         roundtrip_ok=roundtrip,
         per_request_mode=per_request_mode,
     )
+    if other is not None:
+        out["other_path"] = other
     if per_placement:
         out["per_placement"] = per_placement
         for op in ("pack", "unpack"):
@@ -1399,7 +1445,8 @@ def main():
     say("[bench] decode leg (llama3-8b-decode)")
     w = W.c2_llama8b()
     dec = incremental_leg(torch, kv, w, args.steps, args.warmup, seed=2,
-                          placements=args.placements, regions=20)
+                          placements=args.placements, regions=20,
+                          path="ranges", compare="plan")
     dominant = ("pack" if dec["pack_us_mean"] >= dec["unpack_us_mean"]
                 else "unpack")
     achieved = dec[f"{dominant}_GBps"]
@@ -1415,8 +1462,9 @@ def main():
                    "block_size": w.shape.block_size,
                    "cache_layout": w.shape.order, "requests": w.num_reqs,
                    "tokens_per_step_mean": dec["tokens_per_step_mean"],
-                   "step": "plan+pack of step k, plan+unpack of step k+10 "
-                           "(20 checkpoint regions per arena)",
+                   "step": "pack of step k, unpack of step k+10 (20 "
+                           "checkpoint regions per arena), each one launch "
+                           "that plans from the token ranges itself",
                    "placements": dec["placements"],
                    "fingerprint": dec["fingerprint"],
                    "parallelism": "none (1 GPU)"},
@@ -1439,9 +1487,11 @@ def main():
             "per_placement") if k in dec}),
         "roundtrip_ok": dec["roundtrip_ok"],
         "per_request_mode": rounded(dec["per_request_mode"]),
+        "other_path": rounded(dec["other_path"]),
         "roofline": {"bound": "hbm",
-                     "kernel": "copy_rows_kernel<%s, false> (%s)" % (
-                         "true" if dominant == "pack" else "false", dominant),
+                     "kernel": "copy_rows_kernel<%s, false, RangeWalk> (%s)"
+                               % ("true" if dominant == "pack" else "false",
+                                  dominant),
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBPS, 4),

@@ -88,13 +88,20 @@ extern "C" {
 #define LUMEN_ERR_CAPACITY (-7)    /* checkpoint row outside [0, ckpt_rows); host libraries: out of host memory */
 #define LUMEN_ERR_DUP_BLOCK (-8)   /* validate mode: a block named by two
                                       pages that an unpack would write */
-#define LUMEN_ERR_TOO_MANY (-9)    /* lumen_kv_ckpt_pack_noalloc: more than
-                                      LUMEN_KV_CKPT_NOALLOC_MAX_REQS requests */
+#define LUMEN_ERR_TOO_MANY (-9)    /* more requests than the call takes:
+                                      LUMEN_KV_CKPT_NOALLOC_MAX_REQS for
+                                      lumen_kv_ckpt_pack_noalloc,
+                                      LUMEN_KV_CKPT_RANGES_MAX_REQS for the
+                                      _ranges calls */
 
 /* Most requests lumen_kv_ckpt_pack_noalloc takes in one call. */
 #ifndef LUMEN_KV_CKPT_NOALLOC_MAX_REQS
 #define LUMEN_KV_CKPT_NOALLOC_MAX_REQS 16384
 #endif
+
+/* Most requests lumen_kv_ckpt_pack_ranges / _unpack_ranges take in one
+ * call: every wavefront of their launch scans all the ranges itself. */
+#define LUMEN_KV_CKPT_RANGES_MAX_REQS 4096
 
 #define LUMEN_CACHE_NHD 0
 #define LUMEN_CACHE_HND 1
@@ -199,6 +206,50 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
                          int32_t num_reqs, void *d_workspace,
                          const void *d_ckpt, int64_t ckpt_rows,
                          lumen_stream_t stream);
+
+/* Plan and copy in one launch (Sec. 4.2's incremental checkpoint of the
+ * tokens written since the last one, and Sec. 4.3's restore): the same
+ * rows, bytes and device-detected errors as lumen_kv_ckpt_plan(d_start,
+ * d_end, num_reqs, row_base, d_req_row_base, ws, stream) followed by
+ * lumen_kv_ckpt_pack (or _unpack) over ws, but with no workspace and no
+ * plan kernel: each wavefront of the copy scans the ranges (device int32
+ * [num_reqs] each) itself, which saves the plan's launch and the wait for
+ * it on every call.  The token-major walk is used for every layout.
+ *
+ * Status.  d_status is a caller-owned device int32, 4-byte aligned.  A call
+ * only lowers it (atomic minimum) to the most negative code it records and
+ * never sets it back: write LUMEN_OK to it before the first call; it then
+ * holds the most negative code of every call since, once the stream has
+ * passed them, so a loop of steps can check it once.  An invalid range
+ * (start < 0 or end < start) records LUMEN_ERR_RANGE and copies no rows for
+ * that request, as the plan does.
+ *
+ * Host errors (nothing enqueued): those of the plan and the copy, NULL
+ * d_status (INVALID_ARG), d_status not 4-byte aligned (MISALIGNED), and
+ * num_reqs above LUMEN_KV_CKPT_RANGES_MAX_REQS (TOO_MANY).  num_reqs == 0
+ * enqueues nothing and leaves d_status as it is. */
+int lumen_kv_ckpt_pack_ranges(const lumen_kv_layout *layout,
+                              const void *d_cache,
+                              const int32_t *d_block_tables, int32_t bt_cols,
+                              const int32_t *d_start, const int32_t *d_end,
+                              int32_t num_reqs, int64_t row_base,
+                              const int64_t *d_req_row_base, void *d_ckpt,
+                              int64_t ckpt_rows, int32_t *d_status,
+                              lumen_stream_t stream);
+
+/* The inverse of lumen_kv_ckpt_pack_ranges, as lumen_kv_ckpt_unpack is of
+ * lumen_kv_ckpt_pack: checkpoint rows into the planned tokens' slots of
+ * d_cache under d_block_tables; every other byte of d_cache is left
+ * untouched.  Status, limits and errors as lumen_kv_ckpt_pack_ranges. */
+int lumen_kv_ckpt_unpack_ranges(const lumen_kv_layout *layout,
+                                void *d_cache,
+                                const int32_t *d_block_tables,
+                                int32_t bt_cols, const int32_t *d_start,
+                                const int32_t *d_end, int32_t num_reqs,
+                                int64_t row_base,
+                                const int64_t *d_req_row_base,
+                                const void *d_ckpt, int64_t ckpt_rows,
+                                int32_t *d_status, lumen_stream_t stream);
 
 /* Part of a pack, through a window of the checkpoint.  Copies only the
  * plan's packed rows [row_begin, row_end), clipped to the plan's total;

@@ -79,6 +79,18 @@ namespace {
 #ifndef LUMEN_KV_CKPT_MIN_WAVES_PER_CU
 #define LUMEN_KV_CKPT_MIN_WAVES_PER_CU 16
 #endif
+// Spans of the copy grid that each wavefront of the one-launch range walk
+// copies when a (row, layer) unit is 4 KiB or more (the grid then has that
+// many times fewer wavefronts than spans; wavefront w takes spans w, w + n,
+// ...).  Each wavefront's set-up scans the ranges, and on the decode
+// workload (4 KiB units, about one unit per span) two spans per wavefront
+// gave 190.7 against 204.6 us per step with one.  With shorter units (2 KiB,
+// head-major Qwen steps, several units per span) two spans per wavefront
+// were slower (703 against 657 us per pack), so those keep one.  Plans
+// read from a workspace set up in a few loads, and keep one span each.
+#ifndef LUMEN_KV_CKPT_RANGE_SPANS_PER_WAVE
+#define LUMEN_KV_CKPT_RANGE_SPANS_PER_WAVE 2
+#endif
 // Double-buffer the batches of a row segment (1) or not (0).
 #ifndef LUMEN_KV_CKPT_PIPELINE
 #define LUMEN_KV_CKPT_PIPELINE 1
@@ -189,6 +201,7 @@ struct Geom {
   int32_t unit_vecs;    // 16-byte vectors per (token, layer): 2*H*D*E/16
   int32_t bt_cols;
   int32_t num_reqs;
+  int64_t spans;        // spans the units are split into (0: one per wave)
   FastDiv div_unit;     // by unit_vecs
   FastDiv div_kv;       // by H*D*E/16, vectors of one (token, layer, K/V)
   FastDiv div_head;     // by D*E/16, vectors of one head
@@ -367,114 +380,315 @@ __device__ __forceinline__ int row_status(bool past, int32_t entry,
   return LUMEN_OK;
 }
 
+// Where the copy walk finds a token row's request, source token and
+// checkpoint row.  WsWalk reads the plan a plan kernel wrote into the
+// workspace; RangeWalk reads the ranges themselves, and every wavefront
+// scans their token counts on its own, so the copy needs no plan launch
+// before it.  Both give the same rows: the packed rows of request r start at
+// row_base plus the tokens of the valid requests before it; per-request rows
+// start at req_row_base[r] + start[r]; invalid ranges count no tokens.
+struct WsWalk {
+  const WsHeader *hdr;
+  const int64_t *prefix;
+  const int64_t *first_row;
+  const int32_t *start;
+
+  __device__ __forceinline__ WsWalk(const void *p0, const void *p1,
+                                    const void *p2, const void *p3, int64_t)
+      : hdr(static_cast<const WsHeader *>(p0)),
+        prefix(static_cast<const int64_t *>(p1)),
+        first_row(static_cast<const int64_t *>(p2)),
+        start(static_cast<const int32_t *>(p3)) {}
+
+  // Total token rows of the plan; false when the plan does not match the
+  // launch (the wavefront then stops).
+  __device__ __forceinline__ bool init(const Geom &g, int lane, int64_t gw,
+                                       int32_t *err, int64_t &total) {
+    if (hdr->num_reqs != g.num_reqs) {
+      if (gw == 0) record_error(err, LUMEN_ERR_INVALID_ARG);
+      return false;
+    }
+    total = hdr->total_rows;
+    return true;
+  }
+
+  // Request r owning token row `row` (row < total), the end of its rows,
+  // its token and its checkpoint buffer row.  The owner is the last request
+  // whose prefix does not exceed the row (empty requests share their
+  // successor's prefix and are skipped by taking the last).  A 64-way
+  // search, one vector load per level, keeps the chain of dependent loads
+  // before the first copy short (two levels up to 4096 requests).
+  __device__ __forceinline__ void locate(int64_t row, int lane, const Geom &g,
+                                         int32_t &r, int64_t &row_end,
+                                         int64_t &t, int64_t &crow) const {
+    int32_t lo = 0, n = g.num_reqs;
+    while (n > 1) {
+      const int32_t step = (n + kWave - 1) / kWave;
+      const int32_t off = lane * step;
+      const int64_t p = off < n ? prefix[lo + off] : INT64_MAX;
+      const int32_t c = __popcll(__ballot(p <= row));  // >= 1: prefix[lo] <= row
+      lo += (c - 1) * step;
+      n = min(step, n - (c - 1) * step);
+    }
+    r = lo;
+    const int64_t p0 = prefix[r];
+    row_end = prefix[r + 1];
+    t = start[r] + (row - p0);
+    crow = first_row[r] + (row - p0) - g.win_first;  // buffer row
+  }
+
+  // The next request with rows after r2, whose first row is row + 1; one
+  // exists because row + 1 < total.  The bound keeps the walk inside the
+  // plan even if a caller has overwritten the workspace (a valid plan never
+  // reaches it).
+  __device__ __forceinline__ void next(int64_t row, const Geom &g,
+                                       int32_t &r2, int64_t &row_end2,
+                                       int64_t &t2, int64_t &crow2) const {
+    do {
+      ++r2;
+    } while (r2 + 1 < g.num_reqs && prefix[r2 + 1] == row + 1);
+    row_end2 = prefix[r2 + 1];
+    t2 = start[r2];
+    crow2 = first_row[r2] - g.win_first;
+  }
+};
+
+__device__ __forceinline__ int64_t readlane64(int64_t x, int src_lane) {
+  const uint32_t lo =
+      __builtin_amdgcn_readlane(int(uint32_t(uint64_t(x))), src_lane);
+  const uint32_t hi =
+      __builtin_amdgcn_readlane(int(uint32_t(uint64_t(x) >> 32)), src_lane);
+  return int64_t((uint64_t(hi) << 32) | lo);
+}
+
+// x plus its copy from the lane that the DPP control selects (0 where that
+// lane is outside the source row, or the row is masked off), in 64 bits.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ int64_t add_dpp(int64_t x) {
+  const int lo = int(uint32_t(uint64_t(x)));
+  const int hi = int(uint32_t(uint64_t(x) >> 32));
+  const uint32_t ylo = __builtin_amdgcn_update_dpp(0, lo, kCtrl, kRowMask,
+                                                   0xf, true);
+  const uint32_t yhi = __builtin_amdgcn_update_dpp(0, hi, kCtrl, kRowMask,
+                                                   0xf, true);
+  return x + int64_t((uint64_t(yhi) << 32) | ylo);
+}
+
+// Inclusive sum over lanes 0..lane of a full wavefront: shifts by 1, 2, 4
+// and 8 lanes inside each row of 16, then each row's total broadcast to the
+// rows after it (row_bcast:15 to rows 1 and 3, row_bcast:31 to rows 2 and
+// 3).  Cross-lane moves are DPP operand modifiers, with no trip through
+// LDS.
+__device__ __forceinline__ int64_t wave_inclusive_sum(int64_t x) {
+  constexpr int kRowShr = 0x110, kRowBcast15 = 0x142, kRowBcast31 = 0x143;
+  x = add_dpp<kRowShr + 1, 0xf>(x);
+  x = add_dpp<kRowShr + 2, 0xf>(x);
+  x = add_dpp<kRowShr + 4, 0xf>(x);
+  x = add_dpp<kRowShr + 8, 0xf>(x);
+  x = add_dpp<kRowBcast15, 0xa>(x);
+  x = add_dpp<kRowBcast31, 0xc>(x);
+  return x;
+}
+
+__device__ __forceinline__ bool range_ok(int32_t s, int32_t e) {
+  return s >= 0 && e >= s;
+}
+
+// Dynamic LDS of the copy kernel (used by RangeWalk only).
+extern __shared__ __align__(16) int64_t copy_lds[];
+
+struct RangeWalk {
+  const int32_t *start;
+  const int32_t *end;
+  const int64_t *req_row_base;  // null: packed rows from row_base
+  int64_t row_base;
+  // Exclusive prefix of the requests' token counts, prefix[0..R], in LDS:
+  // the workgroup scans the ranges once for its wavefronts.
+  const int64_t *prefix;
+
+  __device__ __forceinline__ RangeWalk(const void *p0, const void *p1,
+                                       const void *p2, const void *,
+                                       int64_t base)
+      : start(static_cast<const int32_t *>(p0)),
+        end(static_cast<const int32_t *>(p1)),
+        req_row_base(static_cast<const int64_t *>(p2)),
+        row_base(base),
+        prefix(copy_lds) {}
+
+  // Thread k of the workgroup sums the token counts of a contiguous chunk
+  // of requests (writing each count to LDS); a wavefront scan and the
+  // wavefronts' totals give each chunk its start; each thread then turns
+  // its counts into prefixes in place.  An invalid range counts no tokens
+  // and is reported once per launch (RANGE), by workgroup 0.
+  __device__ __forceinline__ bool init(const Geom &g, int lane, int64_t,
+                                       int32_t *err, int64_t &total) {
+    int64_t *pre = copy_lds;
+    int64_t *wave_tot = copy_lds + g.num_reqs + 1;  // [kWavesPerBlock]
+    const int tid = threadIdx.x, wave = tid / kWave;
+    const int32_t R = g.num_reqs;
+    const int32_t per = (R + kBlockThreads - 1) / kBlockThreads;
+    const int32_t lo = min(R, tid * per), hi = min(R, lo + per);
+    int64_t local = 0;
+    int bad = 0;
+#pragma unroll 4
+    for (int32_t i = lo; i < hi; ++i) {
+      const int32_t s = start[i], e = end[i];
+      const bool ok = range_ok(s, e);
+      const int64_t n = ok ? int64_t(e) - s : 0;
+      bad |= !ok;
+      pre[i] = n;
+      local += n;
+    }
+    const int64_t incl = wave_inclusive_sum(local);
+    if (lane == kWave - 1) wave_tot[wave] = incl;
+    __syncthreads();
+    int64_t base = 0;
+    total = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      const int64_t x = wave_tot[w];
+      if (w < wave) base += x;
+      total += x;
+    }
+    int64_t run = base + incl - local;
+    for (int32_t i = lo; i < hi; ++i) {
+      const int64_t n = pre[i];
+      pre[i] = run;
+      run += n;
+    }
+    if (tid == 0) pre[R] = total;
+    if (__syncthreads_or(bad) && blockIdx.x == 0 && wave == 0)
+      record_error(err, LUMEN_ERR_RANGE);
+    return true;
+  }
+
+  // As WsWalk::locate, over the prefix in LDS.
+  __device__ __forceinline__ void locate(int64_t row, int lane, const Geom &g,
+                                         int32_t &r, int64_t &row_end,
+                                         int64_t &t, int64_t &crow) const {
+    int32_t lo = 0, n = g.num_reqs;
+    while (n > 1) {
+      const int32_t step = (n + kWave - 1) / kWave;
+      const int32_t off = lane * step;
+      const int64_t p = off < n ? prefix[lo + off] : INT64_MAX;
+      const int32_t c = __popcll(__ballot(p <= row));  // >= 1: prefix[lo] <= row
+      lo += (c - 1) * step;
+      n = min(step, n - (c - 1) * step);
+    }
+    r = lo;
+    const int64_t p0 = readlane64(prefix[r], 0);
+    row_end = readlane64(prefix[r + 1], 0);
+    const int32_t s = start[r];
+    t = s + (row - p0);
+    crow = (req_row_base ? req_row_base[r] + s : row_base + p0) +
+           (row - p0) - g.win_first;
+  }
+
+  // As WsWalk::next, over the prefix in LDS.
+  __device__ __forceinline__ void next(int64_t row, const Geom &g,
+                                       int32_t &r2, int64_t &row_end2,
+                                       int64_t &t2, int64_t &crow2) const {
+    do {
+      ++r2;
+    } while (r2 + 1 < g.num_reqs &&
+             readlane64(prefix[r2 + 1], 0) == row + 1);
+    row_end2 = readlane64(prefix[r2 + 1], 0);
+    t2 = start[r2];
+    crow2 = (req_row_base ? req_row_base[r2] + t2 : row_base + row + 1) -
+            g.win_first;
+  }
+};
+
 // One kernel for both directions.  kPack: cache -> checkpoint;
-// otherwise checkpoint -> cache.
-template <bool kPack, bool kHeadMajor>
+// otherwise checkpoint -> cache.  The walk's arrays come in as separate
+// __restrict__ arguments (p0..p3, in the order of the walk's constructor):
+// only then may the compiler read them with scalar loads, which the
+// stores of the copy could otherwise clobber.
+template <bool kPack, bool kHeadMajor, class Walk>
 __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_kernel(
     const uint8_t *__restrict__ src, uint8_t *__restrict__ dst,
-    const int32_t *__restrict__ block_tables,
-    const WsHeader *__restrict__ hdr, const int64_t *__restrict__ prefix,
-    const int64_t *__restrict__ first_row, const int32_t *__restrict__ start,
-    int32_t *err, Geom g) {
+    const int32_t *__restrict__ block_tables, const void *__restrict__ p0,
+    const void *__restrict__ p1, const void *__restrict__ p2,
+    const void *__restrict__ p3, int64_t row_base, int32_t *err, Geom g) {
+  Walk walk(p0, p1, p2, p3, row_base);
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wave;
   const int64_t nw = int64_t(gridDim.x) * kWavesPerBlock;
 
-  if (hdr->num_reqs != g.num_reqs) {
-    if (gw == 0) record_error(err, LUMEN_ERR_INVALID_ARG);
-    return;
-  }
+  int64_t total;
+  if (!walk.init(g, lane, gw, err, total)) return;
   const int64_t L = g.num_layers;
-  const int64_t total = hdr->total_rows;
   const int64_t row_a = min(g.row_lo, total), row_b = min(g.row_hi, total);
   const int64_t units = (row_b - row_a) * L;
-  int64_t u = row_a * L + units * gw / nw;
-  const int64_t u_end = row_a * L + units * (gw + 1) / nw;
-  if (u >= u_end) return;
+  // The units are split into V equal spans; wave gw copies spans gw,
+  // gw + nw, ... (one span per wave unless the launch asks for fewer waves
+  // than spans, so that each wave's set-up serves several).
+  const int64_t V = g.spans > 0 ? g.spans : nw;
+  for (int64_t v = gw; v < V; v += nw) {
+    int64_t u = row_a * L + units * v / V;
+    const int64_t u_end = row_a * L + units * (v + 1) / V;
+    if (u >= u_end) continue;
 
-  // First token row of the span and the request that owns it: the last
-  // request whose prefix does not exceed the row (empty requests share
-  // their successor's prefix and are skipped by taking the last).  A 64-way
-  // search, one vector load per level, keeps the chain of dependent loads
-  // before the first copy short (two levels up to 4096 requests).
-  int64_t row = u / L;
-  int32_t l0 = int32_t(u - row * L);
-  int32_t lo = 0, n = g.num_reqs;
-  while (n > 1) {
-    const int32_t step = (n + kWave - 1) / kWave;
-    const int32_t off = lane * step;
-    const int64_t p = off < n ? prefix[lo + off] : INT64_MAX;
-    const int32_t c = __popcll(__ballot(p <= row));  // >= 1: prefix[lo] <= row
-    lo += (c - 1) * step;
-    n = min(step, n - (c - 1) * step);
-  }
-  int32_t r = lo;
-  const int64_t p0 = prefix[r];
-  int64_t row_end = prefix[r + 1];
-  int64_t t = start[r] + (row - p0);
-  int64_t crow = first_row[r] + (row - p0) - g.win_first;  // buffer row
-  if (g.bt_cols == 0) {  // every page lies past an empty table
-    record_error(err, LUMEN_ERR_RANGE);
-    return;
-  }
-  bool past;
-  int32_t b = block_tables[entry_index(r, t, g, past)];
-
-  while (true) {
-    const int32_t nl = int32_t(min(int64_t(g.num_layers - l0), u_end - u));
-    const bool more = u + nl < u_end;
-    const int code = row_status(past, b, crow, g);
-    // Cache side: (block, slot) of layer 0 / K; checkpoint side: the span's
-    // first unit in this row.
-    const uint32_t slot = uint32_t(t) - fdiv(uint32_t(t), g.div_bs) *
-                                            uint32_t(g.block_size);
-    const int64_t cache_tok =
-        int64_t(b) * g.block_bytes + int64_t(slot) * g.slot_bytes;
-    const int64_t ckpt_off =
-        crow * g.row_bytes + int64_t(l0) * g.unit_vecs * 16;
-    // Materialise this row's addresses here: otherwise the compiler sinks
-    // their arithmetic below the next row's block-table load, and the wait
-    // for this row's entry then also waits for that load.
-    asm volatile("" ::"s"(cache_tok), "s"(ckpt_off) : "memory");
-
-    // Position and block-table entry of the next row.  The entry is loaded
-    // unconditionally (clamped index), after every use of this row's entry
-    // and before this row's copy, and first used after that copy: the scalar
-    // load overlaps with the copy instead of stalling the next row.
-    int32_t r2 = r;
-    int64_t row_end2 = row_end, t2 = t + 1, crow2 = crow + 1;
-    if (more && row + 1 == row_end) {
-      // Next request with rows; one exists because row + 1 < total_rows.
-      // The bound keeps the walk inside the plan even if a caller has
-      // overwritten the workspace (a valid plan never reaches it).
-      do {
-        ++r2;
-      } while (r2 + 1 < g.num_reqs && prefix[r2 + 1] == row + 1);
-      row_end2 = prefix[r2 + 1];
-      t2 = start[r2];
-      crow2 = first_row[r2] - g.win_first;
+    // First token row of the span and its request.
+    int64_t row = u / L;
+    int32_t l0 = int32_t(u - row * L);
+    int32_t r;
+    int64_t row_end, t, crow;
+    walk.locate(row, lane, g, r, row_end, t, crow);
+    if (g.bt_cols == 0) {  // every page lies past an empty table
+      record_error(err, LUMEN_ERR_RANGE);
+      return;
     }
-    bool past2;
-    const int32_t b2 = block_tables[entry_index(r2, t2, g, past2)];
+    bool past;
+    int32_t b = block_tables[entry_index(r, t, g, past)];
 
-    if (code != LUMEN_OK) {
-      record_error(err, code);
-    } else {
-      copy_segment<kPack, kHeadMajor>(src, dst, cache_tok, ckpt_off,
-                                      uint32_t(l0) * uint32_t(g.unit_vecs),
-                                      nl * g.unit_vecs, lane, g);
+    while (true) {
+      const int32_t nl = int32_t(min(int64_t(g.num_layers - l0), u_end - u));
+      const bool more = u + nl < u_end;
+      const int code = row_status(past, b, crow, g);
+      // Cache side: (block, slot) of layer 0 / K; checkpoint side: the span's
+      // first unit in this row.
+      const uint32_t slot = uint32_t(t) - fdiv(uint32_t(t), g.div_bs) *
+                                              uint32_t(g.block_size);
+      const int64_t cache_tok =
+          int64_t(b) * g.block_bytes + int64_t(slot) * g.slot_bytes;
+      const int64_t ckpt_off =
+          crow * g.row_bytes + int64_t(l0) * g.unit_vecs * 16;
+      // Materialise this row's addresses here: otherwise the compiler sinks
+      // their arithmetic below the next row's block-table load, and the wait
+      // for this row's entry then also waits for that load.
+      asm volatile("" ::"s"(cache_tok), "s"(ckpt_off) : "memory");
+
+      // Position and block-table entry of the next row.  The entry is loaded
+      // unconditionally (clamped index), after every use of this row's entry
+      // and before this row's copy, and first used after that copy: the scalar
+      // load overlaps with the copy instead of stalling the next row.
+      int32_t r2 = r;
+      int64_t row_end2 = row_end, t2 = t + 1, crow2 = crow + 1;
+      if (more && row + 1 == row_end)
+        walk.next(row, g, r2, row_end2, t2, crow2);
+      bool past2;
+      const int32_t b2 = block_tables[entry_index(r2, t2, g, past2)];
+
+      if (code != LUMEN_OK) {
+        record_error(err, code);
+      } else {
+        copy_segment<kPack, kHeadMajor>(src, dst, cache_tok, ckpt_off,
+                                        uint32_t(l0) * uint32_t(g.unit_vecs),
+                                        nl * g.unit_vecs, lane, g);
+      }
+      if (!more) break;
+      u += nl;
+      l0 = 0;
+      ++row;
+      r = r2;
+      row_end = row_end2;
+      t = t2;
+      crow = crow2;
+      b = b2;
+      past = past2;
     }
-    if (!more) break;
-    u += nl;
-    l0 = 0;
-    ++row;
-    r = r2;
-    row_end = row_end2;
-    t = t2;
-    crow = crow2;
-    b = b2;
-    past = past2;
   }
 }
 
@@ -909,6 +1123,11 @@ constexpr int kMaxDevices = 64;
 // (it is a host-side stand-in); each device's address comes from
 // hipGetSymbolAddress at that device's set-up.
 constexpr int32_t kNoAllocMaxReqs = LUMEN_KV_CKPT_NOALLOC_MAX_REQS;
+// The range walk keeps a prefix of 8 bytes per request in each
+// workgroup's LDS (32 KiB at the limit).
+constexpr int32_t kRangesMaxReqs = LUMEN_KV_CKPT_RANGES_MAX_REQS;
+static_assert(sizeof(int64_t) * (kRangesMaxReqs + 1 + kWavesPerBlock) <=
+                  64 * 1024, "range walk LDS");
 constexpr size_t kScratchBytes = ws_bytes(kNoAllocMaxReqs);
 static __device__ __align__(256) uint8_t scratch[kScratchBytes];
 constexpr int32_t kMaxSlots = 64;  // ring slots of a staging pipeline
@@ -1049,17 +1268,60 @@ int check_copy_buffers(const lumen_kv_layout *lay, const void *cache,
 // max_waves > 0 caps the grid (a copy whose checkpoint side is host memory
 // across the host link needs a few hundred wavefronts, not the HBM grid) and
 // keeps the token-major walk, whose checkpoint accesses are sequential.
+template <class Walk>
+void launch_rows(bool pack, bool hnd, unsigned blocks, size_t lds,
+                 hipStream_t s, const uint8_t *in, uint8_t *out,
+                 const int32_t *bt, const void *p0, const void *p1,
+                 const void *p2, const void *p3, int64_t row_base,
+                 int32_t *err, const Geom &g) {
+  const dim3 grid(blocks), block(kBlockThreads);
+  if (pack) {
+    if (hnd)
+      hipLaunchKernelGGL((copy_rows_kernel<true, true, Walk>), grid, block,
+                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
+                         g);
+    else
+      hipLaunchKernelGGL((copy_rows_kernel<true, false, Walk>), grid, block,
+                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
+                         g);
+  } else {
+    if (hnd)
+      hipLaunchKernelGGL((copy_rows_kernel<false, true, Walk>), grid, block,
+                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
+                         g);
+    else
+      hipLaunchKernelGGL((copy_rows_kernel<false, false, Walk>), grid, block,
+                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
+                         g);
+  }
+}
+
+// The ranges of a one-launch copy.
+struct Ranges {
+  const int32_t *start;
+  const int32_t *end;
+  const int64_t *req_row_base;
+  int64_t row_base;
+};
+
+// Copies the rows of a plan: the workspace's (ws) or, with `ranges`, the
+// ranges themselves in a single launch (ws unused, err_word required).
 int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
                 void *dst, const int32_t *bt, int32_t bt_cols,
                 int32_t num_reqs, void *ws, int64_t row_lo, int64_t row_hi,
                 int64_t win_first, int64_t ckpt_rows, lumen_stream_t stream,
-                int64_t max_waves = 0, int32_t *err_word = nullptr) {
+                int64_t max_waves = 0, int32_t *err_word = nullptr,
+                const Ranges *ranges = nullptr) {
   int st = check_layout(lay);
   if (st != LUMEN_OK) return st;
   if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0) return LUMEN_ERR_INVALID_ARG;
   if (row_lo < 0 || row_hi < row_lo || win_first < 0) return LUMEN_ERR_INVALID_ARG;
-  if (!ws) return LUMEN_ERR_INVALID_ARG;
-  if (!aligned16(ws)) return LUMEN_ERR_MISALIGNED;
+  if (ranges) {
+    if (!err_word) return LUMEN_ERR_INVALID_ARG;
+  } else {
+    if (!ws) return LUMEN_ERR_INVALID_ARG;
+    if (!aligned16(ws)) return LUMEN_ERR_MISALIGNED;
+  }
   if (num_reqs == 0 || row_hi == row_lo) return LUMEN_OK;
   st = check_copy_buffers(lay, pack ? src : dst, pack ? dst : src, bt,
                           bt_cols, ckpt_rows);
@@ -1094,7 +1356,7 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   g.div_head = make_fastdiv(uint32_t(d_bytes / 16));
   g.div_bs = make_fastdiv(uint32_t(bs));
 
-  WsView v = ws_view(ws, num_reqs);
+  WsView v = ranges ? WsView{} : ws_view(ws, num_reqs);
   int32_t *err = err_word ? err_word : &v.hdr->err;
   // Oversubscribed grid (waves_per_cu per CU, by unit size), never more
   // waves than the checkpoint buffer could hold units: a wave whose span is
@@ -1119,35 +1381,38 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
     if (pieces < waves) waves = pieces > 0 ? pieces : 1;
   }
   const unsigned blocks = unsigned((waves + kWavesPerBlock - 1) / kWavesPerBlock);
+  // Token-major walk over the ranges: `waves` spans, several of them per
+  // wavefront for long units.
+  unsigned row_blocks = blocks;
+  g.spans = 0;
+  const int64_t spw = LUMEN_KV_CKPT_RANGE_SPANS_PER_WAVE;
+  if (ranges && spw > 1 && g.row_bytes / lay->num_layers >= 4096 &&
+      waves >= 2 * spw) {
+    g.spans = waves;
+    const int64_t phys = (waves + spw - 1) / spw;
+    row_blocks = unsigned((phys + kWavesPerBlock - 1) / kWavesPerBlock);
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint8_t *in = static_cast<const uint8_t *>(src);
   uint8_t *out = static_cast<uint8_t *>(dst);
-  if (pack && !hnd && row_lo == 0 && row_hi == INT64_MAX && win_first == 0 &&
-      max_waves == 0 && use_page_major(H * d_bytes)) {
+  if (ranges) {
+    // LDS: prefix[R + 1] and the wavefronts' totals.
+    const size_t lds = sizeof(int64_t) * (size_t(num_reqs) + 1 + kWavesPerBlock);
+    launch_rows<RangeWalk>(pack, hnd, row_blocks, lds, s, in, out, bt,
+                           ranges->start, ranges->end, ranges->req_row_base,
+                           nullptr, ranges->row_base, err, g);
+  } else if (pack && !hnd && row_lo == 0 && row_hi == INT64_MAX &&
+             win_first == 0 && max_waves == 0 &&
+             use_page_major(H * d_bytes)) {
     hipLaunchKernelGGL(item_scan_kernel, dim3(1), dim3(kPlanThreads), 0, s,
                        v.hdr, v.prefix, v.start, v.items, num_reqs,
                        lay->block_size);
     hipLaunchKernelGGL(pack_pages_kernel, dim3(blocks), dim3(kBlockThreads),
                        0, s, in, out, bt, v.hdr, v.prefix, v.first_row,
                        v.start, v.items, err, g);
-  } else if (pack) {
-    if (hnd)
-      hipLaunchKernelGGL((copy_rows_kernel<true, true>), dim3(blocks),
-                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, err, g);
-    else
-      hipLaunchKernelGGL((copy_rows_kernel<true, false>), dim3(blocks),
-                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, err, g);
   } else {
-    if (hnd)
-      hipLaunchKernelGGL((copy_rows_kernel<false, true>), dim3(blocks),
-                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, err, g);
-    else
-      hipLaunchKernelGGL((copy_rows_kernel<false, false>), dim3(blocks),
-                         dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                         v.prefix, v.first_row, v.start, err, g);
+    launch_rows<WsWalk>(pack, hnd, row_blocks, 0, s, in, out, bt, v.hdr,
+                        v.prefix, v.first_row, v.start, 0, err, g);
   }
   return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
 }
@@ -1282,6 +1547,25 @@ int direct_copy(bool pack, const lumen_kv_layout *layout, const void *cache,
 }
 }  // namespace
 
+// Plan and copy in one launch over the ranges (the _ranges entry points).
+int ranges_copy(bool pack, const lumen_kv_layout *lay, void *cache,
+                const int32_t *bt, int32_t bt_cols, const int32_t *d_start,
+                const int32_t *d_end, int32_t num_reqs, int64_t row_base,
+                const int64_t *d_req_row_base, void *ckpt, int64_t ckpt_rows,
+                int32_t *d_status, lumen_stream_t stream) {
+  int st = check_layout(lay);
+  if (st != LUMEN_OK) return st;
+  if (num_reqs < 0 || bt_cols < 0 || ckpt_rows < 0 || !d_status)
+    return LUMEN_ERR_INVALID_ARG;
+  if (num_reqs > kRangesMaxReqs) return LUMEN_ERR_TOO_MANY;
+  if (reinterpret_cast<uintptr_t>(d_status) & 3) return LUMEN_ERR_MISALIGNED;
+  if (num_reqs > 0 && (!d_start || !d_end)) return LUMEN_ERR_INVALID_ARG;
+  const Ranges ranges{d_start, d_end, d_req_row_base, row_base};
+  return launch_copy(pack, lay, pack ? cache : ckpt, pack ? ckpt : cache, bt,
+                     bt_cols, num_reqs, nullptr, 0, INT64_MAX, 0, ckpt_rows,
+                     stream, 0, d_status, &ranges);
+}
+
 extern "C" {
 
 size_t lumen_kv_ckpt_plan_workspace_bytes(int32_t num_reqs) {
@@ -1363,6 +1647,34 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
   return launch_copy(false, layout, d_ckpt, d_cache, d_block_tables, bt_cols,
                      num_reqs, d_workspace, 0, INT64_MAX, 0, ckpt_rows,
                      stream);
+}
+
+int lumen_kv_ckpt_pack_ranges(const lumen_kv_layout *layout,
+                              const void *d_cache,
+                              const int32_t *d_block_tables, int32_t bt_cols,
+                              const int32_t *d_start, const int32_t *d_end,
+                              int32_t num_reqs, int64_t row_base,
+                              const int64_t *d_req_row_base, void *d_ckpt,
+                              int64_t ckpt_rows, int32_t *d_status,
+                              lumen_stream_t stream) {
+  return ranges_copy(true, layout, const_cast<void *>(d_cache),
+                     d_block_tables, bt_cols, d_start, d_end, num_reqs,
+                     row_base, d_req_row_base, d_ckpt, ckpt_rows, d_status,
+                     stream);
+}
+
+int lumen_kv_ckpt_unpack_ranges(const lumen_kv_layout *layout,
+                                void *d_cache,
+                                const int32_t *d_block_tables,
+                                int32_t bt_cols, const int32_t *d_start,
+                                const int32_t *d_end, int32_t num_reqs,
+                                int64_t row_base,
+                                const int64_t *d_req_row_base,
+                                const void *d_ckpt, int64_t ckpt_rows,
+                                int32_t *d_status, lumen_stream_t stream) {
+  return ranges_copy(false, layout, d_cache, d_block_tables, bt_cols,
+                     d_start, d_end, num_reqs, row_base, d_req_row_base,
+                     const_cast<void *>(d_ckpt), ckpt_rows, d_status, stream);
 }
 
 int lumen_kv_ckpt_pack_rows(const lumen_kv_layout *layout, const void *d_cache,
@@ -1619,7 +1931,7 @@ const char *lumen_kv_ckpt_strerror(int code) {
              "exhausted";
     case LUMEN_ERR_DUP_BLOCK: return "block named by two pages of an unpack";
     case LUMEN_ERR_TOO_MANY:
-      return "more requests than the allocation-free call's scratch holds";
+      return "more requests than the call takes in one launch";
     default: return "unknown status";
   }
 }

@@ -37,6 +37,7 @@ LUMEN_ERR_CAPACITY = -7
 LUMEN_ERR_DUP_BLOCK = -8
 LUMEN_ERR_TOO_MANY = -9
 LUMEN_KV_CKPT_NOALLOC_MAX_REQS = 16384  # include/lumen_kv_ckpt.h
+LUMEN_KV_CKPT_RANGES_MAX_REQS = 4096  # include/lumen_kv_ckpt.h
 LUMEN_CACHE_NHD = 0
 LUMEN_CACHE_HND = 1
 
@@ -88,6 +89,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_pack_noalloc": (ctypes.c_int,
                                        [lay, p, p, i32, p, p, i32, i64, p, p,
                                         i64, p, p]),
+        "lumen_kv_ckpt_pack_ranges": (ctypes.c_int,
+                                      [lay, p, p, i32, p, p, i32, i64, p, p,
+                                       i64, p, p]),
+        "lumen_kv_ckpt_unpack_ranges": (ctypes.c_int,
+                                        [lay, p, p, i32, p, p, i32, i64, p, p,
+                                         i64, p, p]),
         "lumen_kv_ckpt_status": (ctypes.c_int, [p, p]),
         "lumen_kv_ckpt_marks_bytes": (sz, [i64]),
         "lumen_kv_draft_align": (ctypes.c_int,
@@ -344,18 +351,12 @@ def lumen_kv_ckpt_pack(shape, num_blocks: int, cache: torch.Tensor,
           workspace, ckpt, stream)
 
 
-def lumen_kv_ckpt_pack_noalloc(shape, num_blocks: int, cache: torch.Tensor,
-                               block_tables: torch.Tensor,
-                               start: torch.Tensor, end: torch.Tensor,
-                               ckpt: torch.Tensor, status: torch.Tensor,
-                               row_base: int = 0,
-                               req_row_base: Optional[torch.Tensor] = None,
-                               stream: Optional[torch.cuda.Stream] = None
-                               ) -> None:
-    """Plan + pack with the library's own device scratch instead of a
-    workspace (for callers that cannot allocate).  `status` is a device
-    int32 tensor of one element that receives the call's status once the
-    stream has passed it."""
+def _ranges_call(name: str, shape, num_blocks: int, cache: torch.Tensor,
+                 block_tables: torch.Tensor, start: torch.Tensor,
+                 end: torch.Tensor, ckpt: torch.Tensor, status: torch.Tensor,
+                 row_base: int, req_row_base: Optional[torch.Tensor],
+                 stream: Optional[torch.cuda.Stream]) -> None:
+    """Marshals the calls that take the ranges instead of a workspace."""
     R = start.numel()
     if end.numel() != R:
         raise ValueError("start and end differ in length")
@@ -373,14 +374,60 @@ def lumen_kv_ckpt_pack_noalloc(shape, num_blocks: int, cache: torch.Tensor,
             raise ValueError("req_row_base must have one entry per request")
         pb = _dev(req_row_base, "req_row_base", torch.int64)
     lay = layout(shape, num_blocks)
-    _check(load_library().lumen_kv_ckpt_pack_noalloc(
+    _check(getattr(load_library(), name)(
         ctypes.byref(lay), _dev(cache, "cache"),
         _dev(block_tables, "block_tables", torch.int32),
         block_tables.shape[1], _dev(start, "start", torch.int32),
         _dev(end, "end", torch.int32), R, int(row_base), pb,
         _dev(ckpt, "ckpt"), ckpt.numel() // _row_elems(shape),
-        _dev(status, "status", torch.int32), _stream_handle(stream)),
-        "lumen_kv_ckpt_pack_noalloc")
+        _dev(status, "status", torch.int32), _stream_handle(stream)), name)
+
+
+def lumen_kv_ckpt_pack_noalloc(shape, num_blocks: int, cache: torch.Tensor,
+                               block_tables: torch.Tensor,
+                               start: torch.Tensor, end: torch.Tensor,
+                               ckpt: torch.Tensor, status: torch.Tensor,
+                               row_base: int = 0,
+                               req_row_base: Optional[torch.Tensor] = None,
+                               stream: Optional[torch.cuda.Stream] = None
+                               ) -> None:
+    """Plan + pack with the library's own device scratch instead of a
+    workspace (for callers that cannot allocate).  `status` is a device
+    int32 tensor of one element that receives the call's status once the
+    stream has passed it."""
+    _ranges_call("lumen_kv_ckpt_pack_noalloc", shape, num_blocks, cache,
+                 block_tables, start, end, ckpt, status, row_base,
+                 req_row_base, stream)
+
+
+def lumen_kv_ckpt_pack_ranges(shape, num_blocks: int, cache: torch.Tensor,
+                              block_tables: torch.Tensor, start: torch.Tensor,
+                              end: torch.Tensor, ckpt: torch.Tensor,
+                              status: torch.Tensor, row_base: int = 0,
+                              req_row_base: Optional[torch.Tensor] = None,
+                              stream: Optional[torch.cuda.Stream] = None
+                              ) -> None:
+    """Plan and pack in one launch, straight from the ranges.  `status` is
+    a device int32 tensor of one element that the call only lowers to the
+    most negative status it records: set it to 0 (LUMEN_OK) first."""
+    _ranges_call("lumen_kv_ckpt_pack_ranges", shape, num_blocks, cache,
+                 block_tables, start, end, ckpt, status, row_base,
+                 req_row_base, stream)
+
+
+def lumen_kv_ckpt_unpack_ranges(shape, num_blocks: int, cache: torch.Tensor,
+                                block_tables: torch.Tensor,
+                                start: torch.Tensor, end: torch.Tensor,
+                                ckpt: torch.Tensor, status: torch.Tensor,
+                                row_base: int = 0,
+                                req_row_base: Optional[torch.Tensor] = None,
+                                stream: Optional[torch.cuda.Stream] = None
+                                ) -> None:
+    """Plan and unpack in one launch: the inverse of
+    lumen_kv_ckpt_pack_ranges, with the same status rule."""
+    _ranges_call("lumen_kv_ckpt_unpack_ranges", shape, num_blocks, cache,
+                 block_tables, start, end, ckpt, status, row_base,
+                 req_row_base, stream)
 
 
 def lumen_kv_ckpt_unpack(shape, num_blocks: int, cache: torch.Tensor,

@@ -38,10 +38,12 @@ def d2h_words(t: torch.Tensor, elem_bytes: int) -> np.ndarray:
 
 def gpu_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None, dst_pool=None,
              bt_dst=None, row_base=0, req_row_base=None, ckpt_rows=None,
-             in_place=False):
+             in_place=False, via="plan"):
     """Plan + pack (+ unpack) on the GPU.  Returns (status, ckpt, dst_pool)
     as host arrays (dst_pool None when no unpack was asked for).  in_place:
-    the unpack writes into the pool the pack read from."""
+    the unpack writes into the pool the pack read from.  via="plan": the
+    plan kernel into a workspace, then the copies over it; via="ranges":
+    the one-launch copies that read the ranges themselves."""
     s = np.asarray(s, np.int32)
     e = np.asarray(e, np.int32)
     R = s.shape[0]
@@ -51,18 +53,30 @@ def gpu_path(shape, nb_src, src_pool, bt, s, e, nb_dst=None, dst_pool=None,
     eb = shape.elem_bytes
     ck_h = np.full(max(ckpt_rows, 0) * row_elems, SENTINEL, _WORD[eb])
     ck = h2d(ck_h)
-    ws = kv.new_workspace(R, dev())
     rb = None if req_row_base is None else h2d(np.asarray(req_row_base, np.int64))
-    kv.lumen_kv_ckpt_plan(h2d(s), h2d(e), ws, row_base, rb)
+    d_s, d_e = h2d(s), h2d(e)
     src = h2d(src_pool)
-    kv.lumen_kv_ckpt_pack(shape, nb_src, src, h2d(np.asarray(bt, np.int32)),
-                          ws, ck)
+    d_bt = h2d(np.asarray(bt, np.int32))
     dst = None
     if dst_pool is not None:
         dst = src if in_place else h2d(dst_pool)
-        kv.lumen_kv_ckpt_unpack(shape, nb_dst, dst,
-                                h2d(np.asarray(bt_dst, np.int32)), ws, ck)
-    st = kv.lumen_kv_ckpt_status(ws)
+        d_bt2 = h2d(np.asarray(bt_dst, np.int32))
+    if via == "ranges":
+        status = torch.zeros(1, dtype=torch.int32, device=dev())
+        kv.lumen_kv_ckpt_pack_ranges(shape, nb_src, src, d_bt, d_s, d_e, ck,
+                                     status, row_base, rb)
+        if dst is not None:
+            kv.lumen_kv_ckpt_unpack_ranges(shape, nb_dst, dst, d_bt2, d_s,
+                                           d_e, ck, status, row_base, rb)
+        st = int(status.item())
+    else:
+        assert via == "plan", via
+        ws = kv.new_workspace(R, dev())
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws, row_base, rb)
+        kv.lumen_kv_ckpt_pack(shape, nb_src, src, d_bt, ws, ck)
+        if dst is not None:
+            kv.lumen_kv_ckpt_unpack(shape, nb_dst, dst, d_bt2, ws, ck)
+        st = kv.lumen_kv_ckpt_status(ws)
     return (st, d2h_words(ck, eb).reshape(-1, row_elems),
             None if dst is None else d2h_words(dst, eb))
 

@@ -178,6 +178,46 @@ def test_plan_host_validation(lib):
     assert f(FAKE, FAKE, 2, 0, None, FAKE_ODD, None) == kv.LUMEN_ERR_MISALIGNED
 
 
+@pytest.mark.parametrize("fn", ["lumen_kv_ckpt_pack_ranges",
+                                "lumen_kv_ckpt_unpack_ranges"])
+def test_ranges_host_validation(lib, fn):
+    """The one-launch copies refuse bad host arguments before any HIP call,
+    among them a missing or misaligned status word and more requests than
+    one launch's range scan takes."""
+    f = getattr(lib, fn)
+    odd4 = ctypes.c_void_p(0x7F0000000002)  # not 4-byte aligned
+
+    def call(lay=None, cache=FAKE, bt=FAKE, cols=4, s=FAKE, e=FAKE, R=2,
+             ck=FAKE, rows=100, status=FAKE):
+        lay = _layout() if lay is None else lay
+        return f(ctypes.byref(lay), cache, bt, cols, s, e, R, 0, None, ck,
+                 rows, status, None)
+
+    assert call(lay=_layout(num_layers=0)) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(lay=_layout(elem_bytes=3)) == kv.LUMEN_ERR_UNSUPPORTED
+    assert call(R=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(cols=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(rows=-1) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(status=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(R=0, status=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(status=odd4) == kv.LUMEN_ERR_MISALIGNED
+    cap = kv.LUMEN_KV_CKPT_RANGES_MAX_REQS
+    assert call(R=cap + 1) == kv.LUMEN_ERR_TOO_MANY
+    assert call(R=1 << 30) == kv.LUMEN_ERR_TOO_MANY
+    assert call(s=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(e=None) == kv.LUMEN_ERR_INVALID_ARG
+    # no requests: nothing to do, nothing enqueued, whatever the buffers
+    assert call(R=0, s=None, e=None, cache=None, bt=None, ck=None) == \
+        kv.LUMEN_OK
+    assert call(cache=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(bt=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(ck=None) == kv.LUMEN_ERR_INVALID_ARG
+    assert call(cache=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+    assert call(ck=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+    # a status word needs 4-byte alignment only
+    assert call(status=FAKE_ODD, cache=None) == kv.LUMEN_ERR_INVALID_ARG
+
+
 def test_status_and_copies_host_validation(lib):
     assert lib.lumen_kv_ckpt_status(None, None) == kv.LUMEN_ERR_INVALID_ARG
     assert lib.lumen_kv_ckpt_status(FAKE_ODD, None) == kv.LUMEN_ERR_MISALIGNED

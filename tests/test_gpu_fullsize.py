@@ -202,9 +202,14 @@ def free_memory():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("make", [W.c2_llama8b, W.c5_qwen_hnd],
-                         ids=["llama3-8b-decode", "qwen-gqa-hnd"])
-def test_incremental_full_size(make):
+@pytest.mark.parametrize("make,via", [(W.c2_llama8b, "ranges"),
+                                      (W.c2_llama8b, "plan"),
+                                      (W.c5_qwen_hnd, "plan")],
+                         ids=["llama3-8b-decode-ranges",
+                              "llama3-8b-decode-plan", "qwen-gqa-hnd"])
+def test_incremental_full_size(make, via):
+    """via: the copies issued as the benchmark's decode leg issues them (one
+    launch per copy that plans from the ranges) or after a plan kernel."""
     w = make()
     sh = w.shape
     say(f"[fullsize] {w.name}: source pool {w.num_blocks} blocks")
@@ -219,13 +224,22 @@ def test_incremental_full_size(make):
     bt = torch.from_numpy(w.block_tables).to(DEV)
     btd = torch.from_numpy(w.dst_block_tables).to(DEV)
     ws = kv.new_workspace(w.num_reqs, DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
     for k in range(w.num_steps):
         s, e = w.starts[k], w.ends[k]
-        kv.lumen_kv_ckpt_plan(torch.from_numpy(s).to(DEV),
-                              torch.from_numpy(e).to(DEV), ws, int(row_off[k]))
-        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws, arena)
-        kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, btd, ws, arena)
-        assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK, f"step {k}"
+        d_s, d_e = torch.from_numpy(s).to(DEV), torch.from_numpy(e).to(DEV)
+        if via == "ranges":
+            kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, d_s, d_e,
+                                         arena, status, int(row_off[k]))
+            kv.lumen_kv_ckpt_unpack_ranges(sh, w.dst_num_blocks, dst, btd,
+                                           d_s, d_e, arena, status,
+                                           int(row_off[k]))
+            assert int(status.item()) == kv.LUMEN_OK, f"step {k}"
+        else:
+            kv.lumen_kv_ckpt_plan(d_s, d_e, ws, int(row_off[k]))
+            kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws, arena)
+            kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, btd, ws, arena)
+            assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK, f"step {k}"
         check_all_rows(sh, src, w.num_blocks, w.block_tables, s, e, arena,
                        int(row_off[k]), f"{w.name} step {k}")
     say(f"[fullsize] {w.name}: restored pool re-packs to the checkpoint")

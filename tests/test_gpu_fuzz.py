@@ -2,7 +2,8 @@
 (layers, heads, head_dim, block size, element width, NHD or HND), a request
 count, block tables, token ranges (empty ones included), the plan mode
 (packed from a row base, or per-request rows) and a grid size, then checks
-pack, unpack, windowed packs and the direct host copy element by element.
+pack, unpack, windowed packs, the direct host copy and the one-launch copies
+that read the ranges element by element.
 One configuration in eight plants an error (a page past the table, or a
 block id outside the pool); then only the status is compared, since the GPU
 still copies the rows that are fine while the oracle writes nothing."""
@@ -92,9 +93,25 @@ def test_random_configuration_matches_oracle(seed):
     kv.lumen_kv_ckpt_pack(shape, nb, d_src, d_bt, ws, ck_view)
     st_g = kv.lumen_kv_ckpt_status(ws)
     assert st_g == st_o, (seed, st_g, st_o)
+
+    # the one-launch pack and unpack that read the ranges themselves
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+    ck_r = h2d(np.full(max(ck_rows, 1) * re_, SENTINEL, WORD[eb]))
+    kv.lumen_kv_ckpt_pack_ranges(shape, nb, d_src, d_bt, d_s, d_e,
+                                 ck_r[:ck_rows * re_], status,
+                                 0 if per_request else row_base, d_base)
+    assert int(status.item()) == st_o, (seed, "ranges", int(status.item()))
     if st_o != oracle.OK:
         return
     assert np.array_equal(d2h_words(ck_view, eb).reshape(-1, re_), want_ck)
+    assert np.array_equal(
+        d2h_words(ck_r[:ck_rows * re_], eb).reshape(-1, re_), want_ck)
+    d_dst_r = h2d(dst)
+    kv.lumen_kv_ckpt_unpack_ranges(shape, nb, d_dst_r, d_bt2, d_s, d_e,
+                                   ck_view, status,
+                                   0 if per_request else row_base, d_base)
+    assert int(status.item()) == 0
+    assert np.array_equal(d2h_words(d_dst_r, eb), want_dst)
 
     # restore into another pool under the second table
     d_dst = h2d(dst)
@@ -185,5 +202,7 @@ def test_larger_random_shape_matches_oracle(seed):
     else:
         kw = dict(row_base=int(rng.integers(0, 5)))
     args = (shape, nb, src, bt, s, e, nb, dst, bt2)
-    assert_same(gpu_path(*args, **kw), oracle_path(*args, **kw),
-                f"seed {seed}: {shape}, {R} requests")
+    ref = oracle_path(*args, **kw)
+    for via in ("plan", "ranges"):
+        assert_same(gpu_path(*args, **kw, via=via), ref,
+                    f"seed {seed} via {via}: {shape}, {R} requests")

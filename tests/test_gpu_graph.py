@@ -1,6 +1,6 @@
-"""The checkpoint step (plan, pack, plan, unpack) captured in a HIP graph and
-replayed: the library issues only kernels, no memsets, so a capture holds
-the whole step.  Each replay follows eager work that changes the inputs
+"""The checkpoint step (plan, pack, plan, unpack; or the two one-launch
+copies that read the ranges) captured in a HIP graph and replayed: the
+library issues only kernels, no memsets, so a capture holds the whole step.  Each replay follows eager work that changes the inputs
 (new cache contents, a reset destination pool) and a synchronisation, and
 is checked against the oracle on the same inputs."""
 import numpy as np
@@ -20,7 +20,8 @@ pytestmark = pytest.mark.gpu
     lambda: W.c2_llama8b(num_reqs=11, steps=2, median=200, clip_hi=400),
     lambda: W.c4_llama70b_tp8(num_reqs=9, median=150, clip_hi=500),
 ], ids=["decode-small", "tp8-small-page-major"])
-def test_captured_step_replays_match_oracle(make):
+@pytest.mark.parametrize("via", ["plan", "ranges"])
+def test_captured_step_replays_match_oracle(make, via):
     w = make()
     sh = w.shape
     k = 0
@@ -37,17 +38,29 @@ def test_captured_step_replays_match_oracle(make):
     ck = torch.zeros(rows * sh.token_row_elems, dtype=torch.int16,
                      device=dev())
 
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+
     def step():
+        if via == "ranges":
+            kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, d_s, d_e,
+                                         ck, status)
+            kv.lumen_kv_ckpt_unpack_ranges(sh, w.dst_num_blocks, dst, bt2,
+                                           d_s, d_e, ck, status)
+            return
         kv.lumen_kv_ckpt_plan(d_s, d_e, ws_a)
         kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, ck)
         kv.lumen_kv_ckpt_plan(d_s, d_e, ws_b)
         kv.lumen_kv_ckpt_unpack(sh, w.dst_num_blocks, dst, bt2, ws_b, ck)
 
+    def statuses_ok():
+        assert kv.lumen_kv_ckpt_status(ws_a) == 0
+        assert kv.lumen_kv_ckpt_status(ws_b) == 0
+        assert int(status.item()) == 0
+
     # eager once (device state of the library initialised outside capture)
     step()
     torch.cuda.synchronize()
-    assert kv.lumen_kv_ckpt_status(ws_a) == 0
-    assert kv.lumen_kv_ckpt_status(ws_b) == 0
+    statuses_ok()
 
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
@@ -63,8 +76,7 @@ def test_captured_step_replays_match_oracle(make):
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        assert kv.lumen_kv_ckpt_status(ws_a) == 0
-        assert kv.lumen_kv_ckpt_status(ws_b) == 0
+        statuses_ok()
         st, want_ck = oracle.pack(sh, w.num_blocks, new_src, w.block_tables,
                                   s, e)
         assert st == 0

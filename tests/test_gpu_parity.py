@@ -18,6 +18,10 @@ from gpu_util import (SENTINEL, assert_same, gpu_path, oracle_path, h2d,
 
 pytestmark = pytest.mark.gpu
 
+# The two ways to run a plan's copies: the plan kernel into a workspace and
+# the copies over it, or the one-launch copies that read the ranges.
+VIAS = ["plan", "ranges"]
+
 
 def test_smoke():
     import __graft_entry__
@@ -173,27 +177,29 @@ def _case(rng, shape, R, max_tok, incremental, nb_extra=7):
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"L{s.num_layers}H{s.num_kv_heads}D{s.head_dim}bs{s.block_size}{s.order}e{s.elem_bytes}")
 @pytest.mark.parametrize("incremental", [False, True])
-def test_random_shapes(shape, incremental):
+@pytest.mark.parametrize("via", VIAS)
+def test_random_shapes(shape, incremental, via):
     rng = np.random.default_rng(zlib.crc32(f"{shape}{incremental}".encode()))
-    for R, max_tok in ((1, 5), (3, 40), (17, 100)):
+    for R, max_tok in ((1, 5), (3, 40), (17, 100), (70, 30)):
         nb, bt, bt2, s, e, src, dst = _case(rng, shape, R, max_tok,
                                             incremental)
         args = (shape, nb, src, bt, s, e, nb, dst, bt2)
-        assert_same(gpu_path(*args), oracle_path(*args),
+        assert_same(gpu_path(*args, via=via), oracle_path(*args),
                     f"R={R} packed")
         # rows placed after an offset, with spare rows that stay untouched
         n = int((e - s).sum())
         kw = dict(row_base=3, ckpt_rows=n + 6)
-        assert_same(gpu_path(*args, **kw), oracle_path(*args, **kw),
+        assert_same(gpu_path(*args, **kw, via=via), oracle_path(*args, **kw),
                     f"R={R} row_base")
         # per-request reserved regions: token t of r at row base[r] + t
         base = np.arange(R, dtype=np.int64) * (max_tok + 2)
         kw = dict(req_row_base=base, ckpt_rows=R * (max_tok + 2))
-        assert_same(gpu_path(*args, **kw), oracle_path(*args, **kw),
+        assert_same(gpu_path(*args, **kw, via=via), oracle_path(*args, **kw),
                     f"R={R} per-request")
 
 
-def test_empty_plan_and_all_empty_ranges():
+@pytest.mark.parametrize("via", VIAS)
+def test_empty_plan_and_all_empty_ranges(via):
     shape = CacheShape(2, 2, 64, 16, NHD)
     rng = np.random.default_rng(5)
     nb = 8
@@ -202,8 +208,8 @@ def test_empty_plan_and_all_empty_ranges():
     bt = np.arange(8, dtype=np.int32).reshape(4, 2)
     s = np.array([3, 0, 31, 7], np.int32)
     args = (shape, nb, src, bt, s, s, nb, dst, bt)
-    assert_same(gpu_path(*args, ckpt_rows=2), oracle_path(*args, ckpt_rows=2),
-                "all empty")
+    assert_same(gpu_path(*args, ckpt_rows=2, via=via),
+                oracle_path(*args, ckpt_rows=2), "all empty")
 
 
 ERROR_CASES = [
@@ -224,7 +230,8 @@ ERROR_CASES = [
 
 
 @pytest.mark.parametrize("case", range(len(ERROR_CASES)))
-def test_device_error_codes_match_oracle(case):
+@pytest.mark.parametrize("via", VIAS)
+def test_device_error_codes_match_oracle(case, via):
     s, e, bt, rows, base, rb = ERROR_CASES[case]
     shape = CacheShape(2, 2, 8, 4, NHD)
     nb = 8
@@ -235,11 +242,13 @@ def test_device_error_codes_match_oracle(case):
     st_o, _ = oracle.pack(shape, nb, src, bt, s, e, base, rb, ckpt=ck,
                           ckpt_rows=rows)
     st_g, _, _ = gpu_path(shape, nb, src, bt, s, e, row_base=base,
-                          req_row_base=rb, ckpt_rows=rows)
+                          req_row_base=rb, ckpt_rows=rows, via=via)
     assert st_g == st_o, (st_g, st_o)
-    # a fresh plan starts a new error epoch and a clean run reports OK
+    # a fresh plan (or status word) starts a new error epoch and a clean run
+    # reports OK
     st_g, _, _ = gpu_path(shape, nb, src, np.array([[0, 1, 2], [3, 4, 5]],
-                                                   np.int32), [0, 0], [1, 1])
+                                                   np.int32), [0, 0], [1, 1],
+                          via=via)
     assert st_g == kv.LUMEN_OK
 
 
@@ -276,7 +285,8 @@ def _valid_token_rows(shape, nb, bt, s, e, rows, base, rb):
 
 @pytest.mark.parametrize("walk", list(ERROR_WALK_SHAPES))
 @pytest.mark.parametrize("case", range(len(ERROR_CASES)))
-def test_error_inputs_still_copy_every_valid_row(case, walk):
+@pytest.mark.parametrize("via", VIAS)
+def test_error_inputs_still_copy_every_valid_row(case, walk, via):
     """On data-dependent errors only the offending token rows are skipped:
     every other row of the pack equals the oracle's pack of that token
     alone, rows no valid token names keep their sentinel, and the unpack
@@ -310,9 +320,20 @@ def test_error_inputs_still_copy_every_valid_row(case, walk):
     d_rb = None if rb is None else h2d(np.asarray(rb, np.int64))
     d_s, d_e, d_bt = h2d(s), h2d(e), h2d(bt)
     ck = h2d(np.full(rows * shape.token_row_elems, SENTINEL, np.uint16))
-    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, base, d_rb)
-    kv.lumen_kv_ckpt_pack(shape, nb, h2d(src), d_bt, ws, ck)
-    assert kv.lumen_kv_ckpt_status(ws) == st_o
+
+    def copy(pack, cache, ckpt):
+        if via == "ranges":
+            status = torch.zeros(1, dtype=torch.int32, device=dev())
+            fn = (kv.lumen_kv_ckpt_pack_ranges if pack
+                  else kv.lumen_kv_ckpt_unpack_ranges)
+            fn(shape, nb, cache, d_bt, d_s, d_e, ckpt, status, base, d_rb)
+            return int(status.item())
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws, base, d_rb)
+        fn = kv.lumen_kv_ckpt_pack if pack else kv.lumen_kv_ckpt_unpack
+        fn(shape, nb, cache, d_bt, ws, ckpt)
+        return kv.lumen_kv_ckpt_status(ws)
+
+    assert copy(True, h2d(src), ck) == st_o
     got_ck = d2h16(ck).reshape(rows, -1)
     # Overlapping per-request regions (a caller error): the writers of a row
     # two tokens name race, so each element holds one of theirs.
@@ -323,9 +344,7 @@ def test_error_inputs_still_copy_every_valid_row(case, walk):
     assert np.array_equal(got_ck, want_ck), \
         f"{walk}: pack rows differ from the oracle's valid rows"
     d_dst = h2d(dst)
-    kv.lumen_kv_ckpt_plan(d_s, d_e, ws, base, d_rb)
-    kv.lumen_kv_ckpt_unpack(shape, nb, d_dst, d_bt, ws, h2d(ck_in))
-    assert kv.lumen_kv_ckpt_status(ws) == st_o
+    assert copy(False, d_dst, h2d(ck_in)) == st_o
     assert np.array_equal(d2h16(d_dst), want_dst), \
         f"{walk}: unpack wrote other slots than the valid tokens'"
 
@@ -349,7 +368,8 @@ def test_status_clears_the_error_word():
     lambda: W.c2_llama8b(num_reqs=9, steps=3, median=150, clip_hi=300),
     lambda: W.c5_qwen_hnd(num_reqs=13, steps=3, median=100, clip_hi=200),
 ], ids=["llama3-8b-decode-small", "qwen-gqa-hnd-small"])
-def test_reduced_incremental_workloads(make):
+@pytest.mark.parametrize("via", VIAS)
+def test_reduced_incremental_workloads(make, via):
     w = make()
     rng = np.random.default_rng(202)
     src = W.random_bits(rng, w.shape.pool_elems(w.num_blocks))
@@ -357,7 +377,8 @@ def test_reduced_incremental_workloads(make):
     g_dst, o_dst = dst, dst
     for k in range(w.num_steps):
         gpu = gpu_path(w.shape, w.num_blocks, src, w.block_tables, w.starts[k],
-                       w.ends[k], w.dst_num_blocks, g_dst, w.dst_block_tables)
+                       w.ends[k], w.dst_num_blocks, g_dst, w.dst_block_tables,
+                       via=via)
         ref = oracle_path(w.shape, w.num_blocks, src, w.block_tables,
                           w.starts[k], w.ends[k], w.dst_num_blocks, o_dst,
                           w.dst_block_tables)
@@ -365,14 +386,15 @@ def test_reduced_incremental_workloads(make):
         g_dst, o_dst = gpu[2], ref[2]
 
 
-def test_reduced_tp8_shard_in_place():
+@pytest.mark.parametrize("via", VIAS)
+def test_reduced_tp8_shard_in_place(via):
     w = W.c4_llama70b_tp8(num_reqs=11, median=120, clip_hi=400)
     rng = np.random.default_rng(303)
     pool = W.random_bits(rng, w.shape.pool_elems(w.num_blocks))
     # pack, then unpack into the same pool under a fresh permutation
     args = (w.shape, w.num_blocks, pool, w.block_tables, w.starts[0],
             w.ends[0], w.num_blocks, pool, w.dst_block_tables)
-    assert_same(gpu_path(*args, in_place=True), oracle_path(*args),
+    assert_same(gpu_path(*args, in_place=True, via=via), oracle_path(*args),
                 "in place")
 
 
@@ -424,8 +446,10 @@ def test_offload_and_stage_in_bytes():
     assert np.array_equal(got[:500], a[:500]) and not got[500:].any()
 
 
-@pytest.mark.parametrize("R", [1, 63, 64, 65, 1023, 1024, 1025, 5000, 20001])
-def test_plan_many_requests(R):
+@pytest.mark.parametrize("R", [1, 63, 64, 65, 1023, 1024, 1025, 4095, 4096,
+                               5000, 20001])
+@pytest.mark.parametrize("via", VIAS)
+def test_plan_many_requests(R, via):
     """Plans over many requests (several per scan thread, partial
     wavefronts), with empty and invalid ranges sprinkled in; the pack of
     one-element rows checks every planned row against the oracle."""
@@ -439,12 +463,17 @@ def test_plan_many_requests(R):
     empty = rng.random(R) < 0.1
     e[empty] = s[empty]
     src = W.random_bits(rng, shape.pool_elems(nb))
+    if via == "ranges" and R > kv.LUMEN_KV_CKPT_RANGES_MAX_REQS:
+        with pytest.raises(kv.LumenError) as ex:
+            gpu_path(shape, nb, src, bt, s, e, via=via)
+        assert ex.value.code == kv.LUMEN_ERR_TOO_MANY
+        return
     disjoint = np.arange(R, dtype=np.int64) * 20 + rng.integers(0, 5, R)
     for base, rb in ((0, None), (7, None), (0, disjoint)):
         n = int((e - s).sum())
         rows = n + base if rb is None else int(rb.max()) + 13
         gpu = gpu_path(shape, nb, src, bt, s, e, row_base=base,
-                       req_row_base=rb, ckpt_rows=rows)
+                       req_row_base=rb, ckpt_rows=rows, via=via)
         ref = oracle_path(shape, nb, src, bt, s, e, row_base=base,
                           req_row_base=rb, ckpt_rows=rows)
         assert_same(gpu, ref, f"R={R} base={base} per-request={rb is not None}")
@@ -452,7 +481,7 @@ def test_plan_many_requests(R):
     if R > 1:
         s2, e2 = s.copy(), e.copy()
         s2[R // 2], e2[R // 2] = 5, 3
-        st, _, _ = gpu_path(shape, nb, src, bt, s2, e2)
+        st, _, _ = gpu_path(shape, nb, src, bt, s2, e2, via=via)
         assert st == kv.LUMEN_ERR_RANGE
 
 

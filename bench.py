@@ -1160,8 +1160,10 @@ def tiny_leg(torch, kv, W, reps=200):
     so it reports latency: device us of plan + pack and of plan + unpack
     from HIP events around each pair with the stream drained in between,
     the same pairs back to back, and the host cost of enqueueing one call
-    through the binding, also with the calls prepared once (PreparedCall).  Self-check: the restored tokens, packed again
-    from the destination pool, equal the checkpoint."""
+    through the binding, also with the calls prepared once (PreparedCall),
+    and the one-launch range copies prepared the same way.  Self-check:
+    the restored tokens, packed again from the destination pool, equal the
+    checkpoint."""
     dev = torch.device("cuda:0")
     w = W.c1_tiny()
     sh = w.shape
@@ -1215,6 +1217,16 @@ def tiny_leg(torch, kv, W, reps=200):
         p_unpack()
 
     pk_p, up_p = pair_us(pack_prepared), pair_us(unpack_prepared)
+    # one launch per copy, planning from the ranges (prepared the same way)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    p_rpack = kv.prepare_pack_ranges(sh, w.num_blocks, src, bt, s, e, ck,
+                                     status)
+    p_runpack = kv.prepare_unpack_ranges(sh, w.dst_num_blocks, dst, bt2, s,
+                                         e, ck, status)
+    pk_r, up_r = pair_us(p_rpack), pair_us(p_runpack)
+    if int(status.item()) != 0:
+        raise RuntimeError("range copies reported "
+                           f"{kv.lumen_kv_ckpt_strerror(int(status.item()))}")
     torch.cuda.synchronize()
     a = TimingEvent()
     b = TimingEvent()
@@ -1254,6 +1266,8 @@ def tiny_leg(torch, kv, W, reps=200):
             "prepared_plan_pack_us_median": float(np.median(pk_p)),
             "prepared_plan_unpack_us_median": float(np.median(up_p)),
             "prepared_host_enqueue_us_per_call": host_p_us,
+            "prepared_ranges_pack_us_median": float(np.median(pk_r)),
+            "prepared_ranges_unpack_us_median": float(np.median(up_r)),
             "roundtrip_ok": ok}
 
 

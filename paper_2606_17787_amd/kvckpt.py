@@ -351,12 +351,13 @@ def lumen_kv_ckpt_pack(shape, num_blocks: int, cache: torch.Tensor,
           workspace, ckpt, stream)
 
 
-def _ranges_call(name: str, shape, num_blocks: int, cache: torch.Tensor,
+def _ranges_args(shape, num_blocks: int, cache: torch.Tensor,
                  block_tables: torch.Tensor, start: torch.Tensor,
                  end: torch.Tensor, ckpt: torch.Tensor, status: torch.Tensor,
-                 row_base: int, req_row_base: Optional[torch.Tensor],
-                 stream: Optional[torch.cuda.Stream]) -> None:
-    """Marshals the calls that take the ranges instead of a workspace."""
+                 row_base: int, req_row_base: Optional[torch.Tensor]):
+    """(layout struct, argument tuple without the stream) of the calls that
+    take the ranges instead of a workspace; the struct must outlive every
+    use of the tuple."""
     R = start.numel()
     if end.numel() != R:
         raise ValueError("start and end differ in length")
@@ -374,13 +375,53 @@ def _ranges_call(name: str, shape, num_blocks: int, cache: torch.Tensor,
             raise ValueError("req_row_base must have one entry per request")
         pb = _dev(req_row_base, "req_row_base", torch.int64)
     lay = layout(shape, num_blocks)
-    _check(getattr(load_library(), name)(
-        ctypes.byref(lay), _dev(cache, "cache"),
-        _dev(block_tables, "block_tables", torch.int32),
-        block_tables.shape[1], _dev(start, "start", torch.int32),
-        _dev(end, "end", torch.int32), R, int(row_base), pb,
-        _dev(ckpt, "ckpt"), ckpt.numel() // _row_elems(shape),
-        _dev(status, "status", torch.int32), _stream_handle(stream)), name)
+    return lay, (ctypes.byref(lay), _dev(cache, "cache"),
+                 _dev(block_tables, "block_tables", torch.int32),
+                 block_tables.shape[1], _dev(start, "start", torch.int32),
+                 _dev(end, "end", torch.int32), R, int(row_base), pb,
+                 _dev(ckpt, "ckpt"), ckpt.numel() // _row_elems(shape),
+                 _dev(status, "status", torch.int32))
+
+
+def _ranges_call(name: str, shape, num_blocks: int, cache: torch.Tensor,
+                 block_tables: torch.Tensor, start: torch.Tensor,
+                 end: torch.Tensor, ckpt: torch.Tensor, status: torch.Tensor,
+                 row_base: int, req_row_base: Optional[torch.Tensor],
+                 stream: Optional[torch.cuda.Stream]) -> None:
+    """Marshals the calls that take the ranges instead of a workspace."""
+    lay, args = _ranges_args(shape, num_blocks, cache, block_tables, start,
+                             end, ckpt, status, row_base, req_row_base)
+    _check(getattr(load_library(), name)(*args, _stream_handle(stream)), name)
+
+
+def prepare_pack_ranges(shape, num_blocks: int, cache: torch.Tensor,
+                        block_tables: torch.Tensor, start: torch.Tensor,
+                        end: torch.Tensor, ckpt: torch.Tensor,
+                        status: torch.Tensor, row_base: int = 0,
+                        req_row_base: Optional[torch.Tensor] = None
+                        ) -> PreparedCall:
+    """lumen_kv_ckpt_pack_ranges with its arguments checked once; see
+    PreparedCall."""
+    lay, args = _ranges_args(shape, num_blocks, cache, block_tables, start,
+                             end, ckpt, status, row_base, req_row_base)
+    return PreparedCall("lumen_kv_ckpt_pack_ranges", args,
+                        (lay, cache, block_tables, start, end, ckpt, status,
+                         req_row_base))
+
+
+def prepare_unpack_ranges(shape, num_blocks: int, cache: torch.Tensor,
+                          block_tables: torch.Tensor, start: torch.Tensor,
+                          end: torch.Tensor, ckpt: torch.Tensor,
+                          status: torch.Tensor, row_base: int = 0,
+                          req_row_base: Optional[torch.Tensor] = None
+                          ) -> PreparedCall:
+    """lumen_kv_ckpt_unpack_ranges with its arguments checked once; see
+    PreparedCall."""
+    lay, args = _ranges_args(shape, num_blocks, cache, block_tables, start,
+                             end, ckpt, status, row_base, req_row_base)
+    return PreparedCall("lumen_kv_ckpt_unpack_ranges", args,
+                        (lay, cache, block_tables, start, end, ckpt, status,
+                         req_row_base))
 
 
 def lumen_kv_ckpt_pack_noalloc(shape, num_blocks: int, cache: torch.Tensor,

@@ -38,10 +38,12 @@ def test_tiny_workload_full_pack_and_restore():
     assert_same(gpu_path(*args), oracle_path(*args), "tiny")
 
 
-def test_prepared_calls_match_the_oracle():
-    """Plan, pack and unpack prepared once and issued twice on the same
-    buffers, with the token ranges rewritten in place in between (a serving
-    loop's use): each round equals the oracle, and the plain calls."""
+@pytest.mark.parametrize("via", VIAS)
+def test_prepared_calls_match_the_oracle(via):
+    """Plan, pack and unpack (or the one-launch range copies) prepared once
+    and issued twice on the same buffers, with the token ranges rewritten in
+    place in between (a serving loop's use): each round equals the oracle,
+    and the plain calls."""
     w = W.c1_tiny()
     sh = w.shape
     rng = np.random.default_rng(202)
@@ -56,11 +58,23 @@ def test_prepared_calls_match_the_oracle():
     ck = torch.zeros(rows * sh.token_row_elems, dtype=torch.int16,
                      device=dev())
     ws = kv.new_workspace(len(s0), dev())
-    plan = kv.prepare_plan(d_s, d_e, ws)
-    pack = kv.prepare_pack(sh, w.num_blocks, d_src, h2d(w.block_tables), ws,
-                           ck)
-    unpack = kv.prepare_unpack(sh, w.dst_num_blocks, d_dst,
-                               h2d(w.dst_block_tables), ws, ck)
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+    if via == "ranges":
+        pack = kv.prepare_pack_ranges(sh, w.num_blocks, d_src,
+                                      h2d(w.block_tables), d_s, d_e, ck,
+                                      status)
+        unpack = kv.prepare_unpack_ranges(sh, w.dst_num_blocks, d_dst,
+                                          h2d(w.dst_block_tables), d_s, d_e,
+                                          ck, status)
+
+        def plan():
+            pass
+    else:
+        plan = kv.prepare_plan(d_s, d_e, ws)
+        pack = kv.prepare_pack(sh, w.num_blocks, d_src, h2d(w.block_tables),
+                               ws, ck)
+        unpack = kv.prepare_unpack(sh, w.dst_num_blocks, d_dst,
+                                   h2d(w.dst_block_tables), ws, ck)
     want_dst = dst.copy()
     for s, e in ((s0, e0), (s1, e1)):
         d_s.copy_(torch.from_numpy(s))
@@ -68,7 +82,9 @@ def test_prepared_calls_match_the_oracle():
         plan()
         pack()
         unpack()
+        torch.cuda.synchronize()
         assert kv.lumen_kv_ckpt_status(ws) == 0
+        assert int(status.item()) == 0
         n = int((e - s).sum())
         st, want = oracle.pack(sh, w.num_blocks, src, w.block_tables, s, e)
         assert st == oracle.OK

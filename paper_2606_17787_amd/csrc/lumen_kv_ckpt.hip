@@ -382,9 +382,8 @@ __device__ __forceinline__ int row_status(bool past, int32_t entry,
 
 // Where the copy walk finds a token row's request, source token and
 // checkpoint row.  WsWalk reads the plan a plan kernel wrote into the
-// workspace; RangeWalk reads the ranges themselves, and every wavefront
-// scans their token counts on its own, so the copy needs no plan launch
-// before it.  Both give the same rows: the packed rows of request r start at
+// workspace; RangeWalk reads the ranges themselves, each workgroup scanning
+// their token counts into LDS, so the copy needs no plan launch before it.  Both give the same rows: the packed rows of request r start at
 // row_base plus the tokens of the valid requests before it; per-request rows
 // start at req_row_base[r] + start[r]; invalid ranges count no tokens.
 struct WsWalk {

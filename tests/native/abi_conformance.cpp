@@ -180,6 +180,44 @@ static void run_case(const Case &c, uint64_t seed, hipStream_t stream) {
                            stream) == LUMEN_OK);
   CHECK(lumen_kv_ckpt_status(ws, stream) == want_st);
 
+  // The one-launch copies that plan from the ranges themselves: the same
+  // rows and restored pool in both row modes, and the oracle's status for
+  // the bad block id, in a status word the caller clears.
+  int32_t *d_status = dev_copy(std::vector<int32_t>{LUMEN_OK});
+  uint8_t *d_ck3 = nullptr;
+  HIP_OK(hipMalloc(&d_ck3, size_t(total) * row_bytes));
+  uint8_t *d_dst2 = dev_copy(dst);
+  CHECK(lumen_kv_ckpt_pack_ranges(&lay, d_src, d_bt, c.cols, d_s, d_e, c.R, 0,
+                                  nullptr, d_ck3, total, d_status,
+                                  stream) == LUMEN_OK);
+  CHECK(lumen_kv_ckpt_unpack_ranges(&lay, d_dst2, d_bt2, c.cols, d_s, d_e,
+                                    c.R, 0, nullptr, d_ck3, total, d_status,
+                                    stream) == LUMEN_OK);
+  HIP_OK(hipStreamSynchronize(stream));
+  CHECK(host_copy(d_status, 1)[0] == LUMEN_OK);
+  CHECK(host_copy(d_ck3, want.size()) == want);
+  CHECK(host_copy(d_dst2, pool_bytes) == want_dst);
+  uint8_t *d_ck4 = dev_copy(std::vector<uint8_t>(want2.size(), 0xA5));
+  CHECK(lumen_kv_ckpt_pack_ranges(&lay, d_src, d_bt, c.cols, d_s, d_e, c.R, 0,
+                                  d_base, d_ck4, rows2, d_status,
+                                  stream) == LUMEN_OK);
+  HIP_OK(hipStreamSynchronize(stream));
+  CHECK(host_copy(d_status, 1)[0] == LUMEN_OK);
+  CHECK(host_copy(d_ck4, want2.size()) == want2);
+  CHECK(lumen_kv_ckpt_pack_ranges(&lay, d_src, d_bad, c.cols, d_s, d_e, c.R,
+                                  0, nullptr, d_ck3, total, d_status,
+                                  stream) == LUMEN_OK);
+  HIP_OK(hipStreamSynchronize(stream));
+  CHECK(host_copy(d_status, 1)[0] == want_st);
+  CHECK(lumen_kv_ckpt_pack_ranges(&lay, d_src, d_bt, c.cols, d_s, d_e,
+                                  LUMEN_KV_CKPT_RANGES_MAX_REQS + 1, 0,
+                                  nullptr, d_ck3, total, d_status,
+                                  stream) == LUMEN_ERR_TOO_MANY);
+  HIP_OK(hipFree(d_status));
+  HIP_OK(hipFree(d_ck3));
+  HIP_OK(hipFree(d_ck4));
+  HIP_OK(hipFree(d_dst2));
+
   // The direct copy into pinned host memory.
   uint8_t *h_ck = nullptr;
   HIP_OK(hipHostMalloc((void **)&h_ck, size_t(total) * row_bytes,

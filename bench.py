@@ -1387,12 +1387,19 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2606_17787_amd", "csrc",
 def device_code_sha256(path=KERNEL_SRC):
     """sha256 of the device code of the library source: the text from the
     opening of its anonymous namespace up to the marker line that starts
-    the host side (kernels, their helpers and tuning constants)."""
+    the host side (kernels, their helpers and tuning constants), with
+    comments removed and runs of whitespace folded to one space, so that
+    editing a comment does not count as changing the code."""
     import hashlib
+    import re
     text = open(path, "rb").read()
     a = text.index(b"namespace {")
     b = text.index(b"// " + b"-" * 61 + b" host side")
-    return hashlib.sha256(text[a:b]).hexdigest()
+    code = text[a:b].decode()
+    code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+    code = re.sub(r"//[^\n]*", " ", code)
+    code = " ".join(code.split())
+    return hashlib.sha256(code.encode()).hexdigest()
 
 
 def measured_traffic(kernel):

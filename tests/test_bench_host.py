@@ -15,7 +15,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_device_code_hash_tracks_the_kernels_only(tmp_path):
     text = open(bench.KERNEL_SRC).read()
     marker = "// " + "-" * 61 + " host side"
-    a, b = text.index("namespace {"), text.index(marker)
+    a = text.index("namespace {")
+    b = text.index(marker)
     base = tmp_path / "base.hip"
     base.write_text(text)
     h0 = bench.device_code_sha256(str(base))
@@ -26,9 +27,16 @@ def test_device_code_hash_tracks_the_kernels_only(tmp_path):
     head_edit = tmp_path / "head.hip"
     head_edit.write_text("// file header note\n" + text)
     assert bench.device_code_sha256(str(head_edit)) == h0
+    # a comment edited or added among the kernels, or blank lines, do not
+    # count; a line of code does
+    k = text.index("__device__", a)
+    comment_edit = tmp_path / "comment.hip"
+    comment_edit.write_text(text[:k] + "// a note on the kernels\n\n"
+                            + text[k:])
+    assert bench.device_code_sha256(str(comment_edit)) == h0
     kernel_edit = tmp_path / "kernel.hip"
-    mid = (a + b) // 2
-    kernel_edit.write_text(text[:mid] + "\n" + text[mid:])
+    kernel_edit.write_text(text[:k] + "constexpr int kProbe = 1;\n"
+                           + text[k:])
     assert bench.device_code_sha256(str(kernel_edit)) != h0
 
 

@@ -212,9 +212,13 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
  * rows, bytes and device-detected errors as lumen_kv_ckpt_plan(d_start,
  * d_end, num_reqs, row_base, d_req_row_base, ws, stream) followed by
  * lumen_kv_ckpt_pack (or _unpack) over ws, but with no workspace and no
- * plan kernel: each wavefront of the copy scans the ranges (device int32
- * [num_reqs] each) itself, which saves the plan's launch and the wait for
- * it on every call.  The token-major walk is used for every layout.
+ * plan kernel: each workgroup of the copy scans the ranges (device int32
+ * [num_reqs] each) into 8 * (num_reqs + 5) bytes of its LDS, which saves
+ * the plan's launch and the wait for it on every call.  The token-major
+ * walk is used for every layout.  The grid is sized as for
+ * lumen_kv_ckpt_pack; where a (token, layer) unit is 4 KiB or more, it has
+ * half as many wavefronts, each copying two spans of it, so that one scan
+ * serves both.
  *
  * Status.  d_status is a caller-owned device int32, 4-byte aligned.  A call
  * only lowers it (atomic minimum) to the most negative code it records and

@@ -616,3 +616,40 @@ def test_validate_with_an_empty_pool_and_no_requests():
     kv.lumen_kv_ckpt_validate_targets(shape, 8, e.view(0, 2), ws0,
                                       kv.new_marks(8, dev()))
     assert kv.lumen_kv_ckpt_status(ws0) == 0
+
+
+def test_range_copies_on_two_streams_at_once():
+    """The one-launch copies hold no state between calls: two of them in
+    flight at once on two streams, each with its own status word, both
+    equal the oracle."""
+    shape = CacheShape(4, 8, 128, 16, NHD)  # 4 KiB units: two spans a wave
+    rng = np.random.default_rng(909)
+    cases = []
+    for R, max_tok in ((37, 90), (11, 200)):
+        nb, bt, bt2, s, e, src, dst = _case(rng, shape, R, max_tok, True)
+        cases.append((nb, bt, bt2, s, e, src, dst))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = []
+    for (nb, bt, bt2, s, e, src, dst), st in zip(cases, streams):
+        rows = int((e - s).sum())
+        d = dict(ck=h2d(np.full(rows * shape.token_row_elems, SENTINEL,
+                                np.uint16)),
+                 dst=h2d(dst), src=h2d(src), bt=h2d(bt), bt2=h2d(bt2),
+                 s=h2d(s), e=h2d(e),
+                 status=torch.zeros(1, dtype=torch.int32, device=dev()))
+        torch.cuda.synchronize()
+        with torch.cuda.stream(st):
+            kv.lumen_kv_ckpt_pack_ranges(shape, nb, d["src"], d["bt"], d["s"],
+                                         d["e"], d["ck"], d["status"],
+                                         stream=st)
+            kv.lumen_kv_ckpt_unpack_ranges(shape, nb, d["dst"], d["bt2"],
+                                           d["s"], d["e"], d["ck"],
+                                           d["status"], stream=st)
+        outs.append(d)
+    torch.cuda.synchronize()
+    for (nb, bt, bt2, s, e, src, dst), d in zip(cases, outs):
+        st_o, want_ck, want_dst = oracle_path(shape, nb, src, bt, s, e, nb,
+                                              dst, bt2)
+        assert st_o == 0 and int(d["status"].item()) == 0
+        assert np.array_equal(d2h16(d["ck"]).reshape(want_ck.shape), want_ck)
+        assert np.array_equal(d2h16(d["dst"]), want_dst)

@@ -1,9 +1,11 @@
 // Paged KV-cache checkpoint pack / restore unpack for MI355X (gfx950).
 //
 // The operations and layouts are specified in include/lumen_kv_ckpt.h.  This
-// file holds the kernels (row plan, token-major gather and scatter,
-// page-major gather, restore-target validation, draft-state alignment), the
-// staging pipelines to and from pinned host memory, and the C ABI.
+// file holds the kernels (row plan, token-major gather and scatter, with
+// the plan read from a workspace or scanned from the ranges in the same
+// launch, page-major gather, restore-target validation, draft-state
+// alignment), the staging pipelines to and from pinned host memory, and the
+// C ABI.
 //
 // Work decomposition.  A checkpoint is a sequence of token rows, each
 // [L][2][H][D] elements of E bytes (E = 1, 2 or 4; the copy moves raw bits
@@ -29,6 +31,13 @@
 // (token-major cache) or D*E bytes (head-major cache), each a whole number
 // of 128-byte lines for the serving shapes, so every access is full-line and
 // no LDS staging is needed for the head-major transpose.
+//
+// Where the walk finds its plan.  Either a plan kernel has written it into
+// a caller's workspace (the row prefix of every request), or the copy
+// reads the token ranges themselves: each workgroup then scans them into
+// LDS before its wavefronts start, which saves the plan kernel's launch and
+// the wait for it; there, where units are long, each wavefront copies two
+// spans so that one scan serves both.
 
 #include <hip/hip_runtime.h>
 

@@ -653,3 +653,22 @@ def test_range_copies_on_two_streams_at_once():
         assert st_o == 0 and int(d["status"].item()) == 0
         assert np.array_equal(d2h16(d["ck"]).reshape(want_ck.shape), want_ck)
         assert np.array_equal(d2h16(d["dst"]), want_dst)
+
+
+@pytest.mark.parametrize("R", [700, 4096])
+def test_many_requests_with_long_units(R):
+    """Thousands of requests over 4 KiB units: the one-launch copies then
+    scan several requests per thread and copy two spans per wavefront;
+    packed and per-request rows, both paths, against the oracle."""
+    shape = CacheShape(2, 8, 128, 4, NHD)  # 2*8*128*2 = 4 KiB units
+    rng = np.random.default_rng(R)
+    nb, bt, bt2, s, e, src, dst = _case(rng, shape, R, 9, True, nb_extra=3)
+    args = (shape, nb, src, bt, s, e, nb, dst, bt2)
+    ref = oracle_path(*args)
+    base = np.arange(R, dtype=np.int64) * 11 + 2
+    kw = dict(req_row_base=base, ckpt_rows=R * 11 + 13)
+    ref_pr = oracle_path(*args, **kw)
+    for via in VIAS:
+        assert_same(gpu_path(*args, via=via), ref, f"R={R} packed {via}")
+        assert_same(gpu_path(*args, **kw, via=via), ref_pr,
+                    f"R={R} per-request {via}")

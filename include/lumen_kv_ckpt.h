@@ -214,11 +214,14 @@ int lumen_kv_ckpt_unpack(const lumen_kv_layout *layout, void *d_cache,
  * lumen_kv_ckpt_pack (or _unpack) over ws, but with no workspace and no
  * plan kernel: each workgroup of the copy scans the ranges (device int32
  * [num_reqs] each) into 8 * (num_reqs + 5) bytes of its LDS, which saves
- * the plan's launch and the wait for it on every call.  The token-major
- * walk is used for every layout.  The grid is sized as for
- * lumen_kv_ckpt_pack; where a (token, layer) unit is 4 KiB or more, it has
- * half as many wavefronts, each copying two spans of it, so that one scan
- * serves both.
+ * the plan's launch and the wait for it on every call.  The walk is
+ * lumen_kv_ckpt_pack's: page by page for a pack of a token-major cache
+ * with token runs of at most 512 bytes (for up to 2,048 requests; the
+ * page-major walk keeps token and page prefixes, 16 * (num_reqs + 5) bytes
+ * of LDS), token by token otherwise.  The grid is sized as for
+ * lumen_kv_ckpt_pack; where a (token, layer) unit of the token-major walk
+ * is 4 KiB or more, it has half as many wavefronts, each copying two spans
+ * of it, so that one scan serves both.
  *
  * Status.  d_status is a caller-owned device int32, 4-byte aligned.  A call
  * only lowers it (atomic minimum) to the most negative code it records and

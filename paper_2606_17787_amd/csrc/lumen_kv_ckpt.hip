@@ -770,6 +770,153 @@ __device__ __forceinline__ int32_t find_owner(const int64_t *__restrict__ pre,
   return lo;
 }
 
+// Where the page-major pack finds its plan: the (request, page) items and
+// each request's rows.  WsPages reads the workspace (the plan kernel's row
+// prefix and the item scan's items); RangePages scans the ranges into LDS,
+// the token and page counts of every request side by side.
+struct WsPages {
+  const WsHeader *hdr;
+  const int64_t *prefix;
+  const int64_t *first_row;
+  const int32_t *start;
+  const int64_t *items;
+
+  __device__ __forceinline__ WsPages(const void *p0, const void *p1,
+                                     const void *p2, const void *p3,
+                                     const void *p4, int64_t)
+      : hdr(static_cast<const WsHeader *>(p0)),
+        prefix(static_cast<const int64_t *>(p1)),
+        first_row(static_cast<const int64_t *>(p2)),
+        start(static_cast<const int32_t *>(p3)),
+        items(static_cast<const int64_t *>(p4)) {}
+
+  // Total items of the plan; false when the plan does not match the launch.
+  __device__ __forceinline__ bool init(const Geom &g, int64_t gw,
+                                       int32_t *err, int64_t &total) {
+    if (hdr->num_reqs != g.num_reqs) {
+      if (gw == 0) record_error(err, LUMEN_ERR_INVALID_ARG);
+      return false;
+    }
+    total = hdr->total_items;
+    return true;
+  }
+  __device__ __forceinline__ const int64_t *item_prefix() const {
+    return items;
+  }
+  __device__ __forceinline__ int64_t item0(int32_t r) const {
+    return items[r];
+  }
+  // Request r's first token, token count and checkpoint row of its first
+  // token (r has rows: it owns an item).
+  __device__ __forceinline__ void request(int32_t r, const Geom &,
+                                          int64_t &s, int64_t &n,
+                                          int64_t &first) const {
+    s = start[r];
+    n = prefix[r + 1] - prefix[r];
+    first = first_row[r];
+  }
+};
+
+struct RangePages {
+  const int32_t *start;
+  const int32_t *end;
+  const int64_t *req_row_base;  // null: packed rows from row_base
+  int64_t row_base;
+  const int64_t *rows;   // LDS: exclusive prefix of token counts, [R+1]
+  const int64_t *items;  // LDS: exclusive prefix of page counts, [R+1]
+
+  __device__ __forceinline__ RangePages(const void *p0, const void *p1,
+                                        const void *p2, const void *,
+                                        const void *, int64_t base)
+      : start(static_cast<const int32_t *>(p0)),
+        end(static_cast<const int32_t *>(p1)),
+        req_row_base(static_cast<const int64_t *>(p2)),
+        row_base(base),
+        rows(nullptr),
+        items(nullptr) {}
+
+  // As RangeWalk::init, for the token and the page counts at once.
+  __device__ __forceinline__ bool init(const Geom &g, int64_t,
+                                       int32_t *err, int64_t &total) {
+    const int32_t R = g.num_reqs;
+    int64_t *pr = copy_lds;
+    int64_t *pi = copy_lds + (R + 1);
+    int64_t *wave_tot = copy_lds + 2 * (R + 1);  // [2][kWavesPerBlock]
+    rows = pr;
+    items = pi;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int32_t per = (R + kBlockThreads - 1) / kBlockThreads;
+    const int32_t lo = min(R, tid * per), hi = min(R, lo + per);
+    int64_t ln = 0, lp = 0;
+    int bad = 0;
+#pragma unroll 4
+    for (int32_t i = lo; i < hi; ++i) {
+      const int32_t s = start[i], e = end[i];
+      const bool ok = range_ok(s, e);
+      const int64_t n = ok ? int64_t(e) - s : 0;
+      // pages (s + n - 1)/bs - s/bs + 1 of a non-empty range; s + n - 1
+      // < 2^31, in the fast division's range
+      const int64_t np =
+          n > 0 ? int64_t(fdiv(uint32_t(s + n - 1), g.div_bs)) -
+                      int64_t(fdiv(uint32_t(s), g.div_bs)) + 1
+                : 0;
+      bad |= !ok;
+      pr[i] = n;
+      pi[i] = np;
+      ln += n;
+      lp += np;
+    }
+    const int64_t in_n = wave_inclusive_sum(ln);
+    const int64_t in_p = wave_inclusive_sum(lp);
+    if (lane == kWave - 1) {
+      wave_tot[wave] = in_n;
+      wave_tot[kWavesPerBlock + wave] = in_p;
+    }
+    __syncthreads();
+    int64_t bn = 0, bp = 0, tn = 0, tp = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      const int64_t xn = wave_tot[w], xp = wave_tot[kWavesPerBlock + w];
+      if (w < wave) {
+        bn += xn;
+        bp += xp;
+      }
+      tn += xn;
+      tp += xp;
+    }
+    int64_t rn = bn + in_n - ln, rp = bp + in_p - lp;
+    for (int32_t i = lo; i < hi; ++i) {
+      const int64_t n = pr[i], np = pi[i];
+      pr[i] = rn;
+      pi[i] = rp;
+      rn += n;
+      rp += np;
+    }
+    if (tid == 0) {
+      pr[R] = tn;
+      pi[R] = tp;
+    }
+    if (__syncthreads_or(bad) && blockIdx.x == 0 && wave == 0)
+      record_error(err, LUMEN_ERR_RANGE);
+    total = tp;
+    return true;
+  }
+  __device__ __forceinline__ const int64_t *item_prefix() const {
+    return items;
+  }
+  __device__ __forceinline__ int64_t item0(int32_t r) const {
+    return readlane64(items[r], 0);
+  }
+  __device__ __forceinline__ void request(int32_t r, const Geom &g,
+                                          int64_t &s, int64_t &n,
+                                          int64_t &first) const {
+    s = start[r];
+    const int64_t p0 = readlane64(rows[r], 0);
+    n = readlane64(rows[r + 1], 0) - p0;
+    first = req_row_base ? req_row_base[r] + s : row_base + p0;
+  }
+};
+
 // Page-major pack, step 2, for token-major caches whose per-token run
 // (H*D*E bytes per layer and K/V) is short: the unit is one (item, layer),
 // the item's tokens of one page.  Its K run and V run are each one
@@ -781,25 +928,25 @@ __device__ __forceinline__ int32_t find_owner(const int64_t *__restrict__ pre,
 // (256-byte runs): 6.28 TB/s, where contiguous spans per wavefront scatter
 // the concurrent writes over the whole checkpoint and reach 5.1 TB/s, and
 // the token-major walk 5.35 TB/s.
+template <class Pages>
 __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void
 pack_pages_kernel(const uint8_t *__restrict__ cache, uint8_t *__restrict__ ckpt,
                   const int32_t *__restrict__ block_tables,
-                  const WsHeader *__restrict__ hdr,
-                  const int64_t *__restrict__ prefix,
-                  const int64_t *__restrict__ first_row,
-                  const int32_t *__restrict__ start,
-                  const int64_t *__restrict__ items, int32_t *err, Geom g) {
+                  const void *__restrict__ p0, const void *__restrict__ p1,
+                  const void *__restrict__ p2, const void *__restrict__ p3,
+                  const void *__restrict__ p4, int64_t row_base, int32_t *err,
+                  Geom g) {
+  Pages pages(p0, p1, p2, p3, p4, row_base);
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wave;
   const int64_t nw = int64_t(gridDim.x) * kWavesPerBlock;
-  if (hdr->num_reqs != g.num_reqs) {
-    if (gw == 0) record_error(err, LUMEN_ERR_INVALID_ARG);
-    return;
-  }
+  int64_t total_items;
+  if (!pages.init(g, gw, err, total_items)) return;
+  const int64_t *items = pages.item_prefix();
   const int32_t G = g.page_layers;
   const int64_t groups = (g.num_layers + G - 1) / G;
-  const int64_t units = hdr->total_items * groups;
+  const int64_t units = total_items * groups;
   const int32_t tok = g.slot_bytes;  // H*D*E
   const int32_t vpt = tok / 16;
   for (int64_t u = gw; u < units; u += nw) {
@@ -807,13 +954,14 @@ pack_pages_kernel(const uint8_t *__restrict__ cache, uint8_t *__restrict__ ckpt,
     const int32_t l_first = int32_t(u - item * groups) * G;
     const int32_t l_end = min(l_first + G, g.num_layers);
     const int32_t r = find_owner(items, g.num_reqs, item, lane);
-    const int64_t s = start[r];
-    const int64_t e = s + (prefix[r + 1] - prefix[r]);
-    const int64_t j = s / g.block_size + (item - items[r]);
+    int64_t s, n, first;
+    pages.request(r, g, s, n, first);
+    const int64_t e = s + n;
+    const int64_t j = s / g.block_size + (item - pages.item0(r));
     const int64_t t_lo = max(s, j * g.block_size);
     const int64_t t_hi = min(e, (j + 1) * g.block_size);
     const int32_t nt = int32_t(t_hi - t_lo);
-    const int64_t row0 = first_row[r] + (t_lo - s) - g.win_first;
+    const int64_t row0 = first + (t_lo - s) - g.win_first;
     // The item's rows are consecutive: the ones inside the buffer are the
     // tokens [ta, tb) of the page; the others are CAPACITY errors and only
     // they are skipped.
@@ -1134,6 +1282,13 @@ constexpr int32_t kNoAllocMaxReqs = LUMEN_KV_CKPT_NOALLOC_MAX_REQS;
 // The range walk keeps a prefix of 8 bytes per request in each
 // workgroup's LDS (32 KiB at the limit).
 constexpr int32_t kRangesMaxReqs = LUMEN_KV_CKPT_RANGES_MAX_REQS;
+// The page-major pack over the ranges keeps two prefixes (tokens and
+// pages) in LDS; above this many requests the range path packs
+// token-major instead.
+constexpr int32_t kRangesPageMaxReqs = 2048;
+static_assert(sizeof(int64_t) * (2 * (kRangesPageMaxReqs + 1) +
+                                 2 * kWavesPerBlock) <= 64 * 1024,
+              "page-major range walk LDS");
 static_assert(sizeof(int64_t) * (kRangesMaxReqs + 1 + kWavesPerBlock) <=
                   64 * 1024, "range walk LDS");
 constexpr size_t kScratchBytes = ws_bytes(kNoAllocMaxReqs);
@@ -1403,21 +1558,31 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint8_t *in = static_cast<const uint8_t *>(src);
   uint8_t *out = static_cast<uint8_t *>(dst);
-  if (ranges) {
+  const bool page_major = pack && !hnd && row_lo == 0 &&
+                          row_hi == INT64_MAX && win_first == 0 &&
+                          max_waves == 0 && use_page_major(H * d_bytes);
+  if (ranges && page_major && num_reqs <= kRangesPageMaxReqs) {
+    // LDS: the token and page prefixes, [R + 1] each, and the wavefronts'
+    // totals of both.
+    const size_t lds =
+        sizeof(int64_t) * (2 * (size_t(num_reqs) + 1) + 2 * kWavesPerBlock);
+    hipLaunchKernelGGL((pack_pages_kernel<RangePages>), dim3(blocks),
+                       dim3(kBlockThreads), lds, s, in, out, bt,
+                       ranges->start, ranges->end, ranges->req_row_base,
+                       nullptr, nullptr, ranges->row_base, err, g);
+  } else if (ranges) {
     // LDS: prefix[R + 1] and the wavefronts' totals.
     const size_t lds = sizeof(int64_t) * (size_t(num_reqs) + 1 + kWavesPerBlock);
     launch_rows<RangeWalk>(pack, hnd, row_blocks, lds, s, in, out, bt,
                            ranges->start, ranges->end, ranges->req_row_base,
                            nullptr, ranges->row_base, err, g);
-  } else if (pack && !hnd && row_lo == 0 && row_hi == INT64_MAX &&
-             win_first == 0 && max_waves == 0 &&
-             use_page_major(H * d_bytes)) {
+  } else if (page_major) {
     hipLaunchKernelGGL(item_scan_kernel, dim3(1), dim3(kPlanThreads), 0, s,
                        v.hdr, v.prefix, v.start, v.items, num_reqs,
                        lay->block_size);
-    hipLaunchKernelGGL(pack_pages_kernel, dim3(blocks), dim3(kBlockThreads),
-                       0, s, in, out, bt, v.hdr, v.prefix, v.first_row,
-                       v.start, v.items, err, g);
+    hipLaunchKernelGGL((pack_pages_kernel<WsPages>), dim3(blocks),
+                       dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
+                       v.prefix, v.first_row, v.start, v.items, 0, err, g);
   } else {
     launch_rows<WsWalk>(pack, hnd, row_blocks, 0, s, in, out, bt, v.hdr,
                         v.prefix, v.first_row, v.start, 0, err, g);

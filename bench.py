@@ -187,7 +187,7 @@ def _kernel_stats(byts, ms):
 
 def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                     placements=1, regions=None, placement_steps=24,
-                    path="plan", compare=None):
+                    path="plan", compare=None, per_request_path=None):
     """Decode loop: step i packs step k = i mod S into its checkpoint region
     and restores step k + lag from the region packed lag steps earlier (lag =
     half the regions), so the restore never reads a copy still held in the
@@ -209,7 +209,9 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     path: how a step's copies are issued: "plan" (a plan kernel into a
     workspace before each copy) or "ranges" (each copy one launch that
     plans from the ranges itself).  compare: the other path, timed the
-    same way right after on the same buffers (reported as other_path)."""
+    same way right after on the same buffers (reported as other_path).
+    per_request_path: the path of the per-request row mode (default:
+    path)."""
     dev = torch.device("cuda:0")
     sh = w.shape
     S = w.num_steps
@@ -414,10 +416,12 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     assert kv.lumen_kv_ckpt_status(ws_a) == 0
     pr_steps = max(steps // 2, MIN_KERNEL_SAMPLES)
 
+    pr_path = per_request_path or path
+
     def step_pr(i, events=None):
         k = i % NR
         k2 = (k + lag) % NR
-        copies(path, k, k2, dst, arena, events, rrb)
+        copies(pr_path, k, k2, dst, arena, events, rrb)
         return k, k2
 
     for i in range(warmup):
@@ -450,7 +454,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                              back.view(torch.int16)))
     assert kv.lumen_kv_ckpt_status(ws_a) == 0
     per_request_mode = dict(
-        steps=pr_steps, ms_per_step=(t3 - t2) * 1e3 / pr_steps,
+        path=pr_path, steps=pr_steps, ms_per_step=(t3 - t2) * 1e3 / pr_steps,
         step_GBps=gb(pr_step_b) / (t3 - t2),
         pack_GBps=pr_pack["GBps"], unpack_GBps=pr_unpack["GBps"],
         pack_us_median=pr_pack["us_median"],
@@ -1467,7 +1471,8 @@ def main():
     w = W.c2_llama8b()
     dec = incremental_leg(torch, kv, w, args.steps, args.warmup, seed=2,
                           placements=args.placements, regions=20,
-                          path="ranges", compare="plan")
+                          path="ranges", compare="plan",
+                          per_request_path="plan")
     dominant = ("pack" if dec["pack_us_mean"] >= dec["unpack_us_mean"]
                 else "unpack")
     achieved = dec[f"{dominant}_GBps"]

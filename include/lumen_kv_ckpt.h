@@ -16,6 +16,12 @@
  *   unpack  scatter of checkpoint rows into the blocks a new block table
  *           names (loading the checkpointed pages back into GPU memory,
  *           Sec. 4.3)
+ *   pack_ranges / unpack_ranges
+ *           plan and pack (unpack) in one launch, straight from the token
+ *           ranges, with no workspace: the copy plans its rows itself
+ *   pack_noalloc
+ *           plan and pack with the library's own device scratch, for
+ *           callers that cannot allocate
  *   offload / stage_in
  *           device->pinned-host and pinned-host->device copies of packed
  *           rows on a side stream, ordered after (before) the main stream's
@@ -62,7 +68,9 @@
  * word: the offending token rows are skipped, all other rows are still
  * copied, and the word keeps the most negative code seen.  lumen_kv_ckpt_plan
  * starts a new error epoch (it overwrites the word with its own result);
- * lumen_kv_ckpt_status reads and clears it.
+ * lumen_kv_ckpt_status reads and clears it.  The calls without a workspace
+ * (_ranges, _noalloc) record the same codes in a caller-owned status word
+ * instead, as their comments say.
  */
 #ifndef LUMEN_KV_CKPT_H
 #define LUMEN_KV_CKPT_H

@@ -66,7 +66,8 @@
  * (negative codes) and nothing is enqueued.  Errors that depend on device
  * data (ranges, block ids, capacity) are recorded in the workspace's error
  * word: the offending token rows are skipped, all other rows are still
- * copied, and the word keeps the most negative code seen.  lumen_kv_ckpt_plan
+ * copied, and the word keeps the most negative code seen.  (The one
+ * exception is a copy past LUMEN_KV_CKPT_MAX_UNITS, which copies nothing.)  lumen_kv_ckpt_plan
  * starts a new error epoch (it overwrites the word with its own result);
  * lumen_kv_ckpt_status reads and clears it.  The calls without a workspace
  * (_ranges, _noalloc) record the same codes in a caller-owned status word
@@ -100,7 +101,9 @@ extern "C" {
                                       LUMEN_KV_CKPT_NOALLOC_MAX_REQS for
                                       lumen_kv_ckpt_pack_noalloc,
                                       LUMEN_KV_CKPT_RANGES_MAX_REQS for the
-                                      _ranges calls */
+                                      _ranges calls; recorded by a copy
+                                      whose ranges hold more than
+                                      LUMEN_KV_CKPT_MAX_UNITS units */
 
 /* Most requests lumen_kv_ckpt_pack_noalloc takes in one call. */
 #ifndef LUMEN_KV_CKPT_NOALLOC_MAX_REQS
@@ -108,8 +111,18 @@ extern "C" {
 #endif
 
 /* Most requests lumen_kv_ckpt_pack_ranges / _unpack_ranges take in one
- * call: every wavefront of their launch scans all the ranges itself. */
+ * call: every workgroup of their launch scans all the ranges into LDS. */
 #define LUMEN_KV_CKPT_RANGES_MAX_REQS 4096
+
+/* Most (token row, layer) units one copy launch walks.  A copy whose
+ * ranges hold more (their token rows times num_layers; for the calls that
+ * take a row window, the rows inside the window) records LUMEN_ERR_TOO_MANY
+ * and copies nothing.  No checkpoint in device memory comes near it: 2^40
+ * units of the smallest unit (32 bytes) are 32 TiB.  It keeps a malformed
+ * call, such as ends of INT32_MAX on thousands of requests, from holding
+ * the GPU for minutes over rows that are all invalid, and keeps the
+ * launch's 64-bit index arithmetic in range. */
+#define LUMEN_KV_CKPT_MAX_UNITS ((int64_t)1 << 40)
 
 #define LUMEN_CACHE_NHD 0
 #define LUMEN_CACHE_HND 1

@@ -211,6 +211,7 @@ struct Geom {
   int32_t bt_cols;
   int32_t num_reqs;
   int64_t spans;        // spans the units are split into (0: one per wave)
+  int64_t max_rows;     // rows one launch walks at most: max units / L
   FastDiv div_unit;     // by unit_vecs
   FastDiv div_kv;       // by H*D*E/16, vectors of one (token, layer, K/V)
   FastDiv div_head;     // by D*E/16, vectors of one head
@@ -628,6 +629,11 @@ __global__ __launch_bounds__(kBlockThreads) LUMEN_COPY_OCCUPANCY void copy_rows_
   if (!walk.init(g, lane, gw, err, total)) return;
   const int64_t L = g.num_layers;
   const int64_t row_a = min(g.row_lo, total), row_b = min(g.row_hi, total);
+  // More rows than a launch walks: refused as a whole (nothing copied).
+  if (row_b - row_a > g.max_rows) {
+    if (gw == 0) record_error(err, LUMEN_ERR_TOO_MANY);
+    return;
+  }
   const int64_t units = (row_b - row_a) * L;
   // The units are split into V equal spans; wave gw copies spans gw,
   // gw + nw, ... (one span per wave unless the launch asks for fewer waves
@@ -790,14 +796,17 @@ struct WsPages {
         start(static_cast<const int32_t *>(p3)),
         items(static_cast<const int64_t *>(p4)) {}
 
-  // Total items of the plan; false when the plan does not match the launch.
+  // Total items and token rows of the plan; false when the plan does not
+  // match the launch.
   __device__ __forceinline__ bool init(const Geom &g, int64_t gw,
-                                       int32_t *err, int64_t &total) {
+                                       int32_t *err, int64_t &total,
+                                       int64_t &rows_total) {
     if (hdr->num_reqs != g.num_reqs) {
       if (gw == 0) record_error(err, LUMEN_ERR_INVALID_ARG);
       return false;
     }
     total = hdr->total_items;
+    rows_total = hdr->total_rows;
     return true;
   }
   __device__ __forceinline__ const int64_t *item_prefix() const {
@@ -837,7 +846,8 @@ struct RangePages {
 
   // As RangeWalk::init, for the token and the page counts at once.
   __device__ __forceinline__ bool init(const Geom &g, int64_t,
-                                       int32_t *err, int64_t &total) {
+                                       int32_t *err, int64_t &total,
+                                       int64_t &rows_total) {
     const int32_t R = g.num_reqs;
     int64_t *pr = copy_lds;
     int64_t *pi = copy_lds + (R + 1);
@@ -899,6 +909,7 @@ struct RangePages {
     if (__syncthreads_or(bad) && blockIdx.x == 0 && wave == 0)
       record_error(err, LUMEN_ERR_RANGE);
     total = tp;
+    rows_total = tn;
     return true;
   }
   __device__ __forceinline__ const int64_t *item_prefix() const {
@@ -941,8 +952,13 @@ pack_pages_kernel(const uint8_t *__restrict__ cache, uint8_t *__restrict__ ckpt,
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t gw = int64_t(blockIdx.x) * kWavesPerBlock + wave;
   const int64_t nw = int64_t(gridDim.x) * kWavesPerBlock;
-  int64_t total_items;
-  if (!pages.init(g, gw, err, total_items)) return;
+  int64_t total_items, total_rows;
+  if (!pages.init(g, gw, err, total_items, total_rows)) return;
+  // The limit of the token-major walk, on the same rows.
+  if (total_rows > g.max_rows) {
+    if (gw == 0) record_error(err, LUMEN_ERR_TOO_MANY);
+    return;
+  }
   const int64_t *items = pages.item_prefix();
   const int32_t G = g.page_layers;
   const int64_t groups = (g.num_layers + G - 1) / G;
@@ -983,33 +999,33 @@ pack_pages_kernel(const uint8_t *__restrict__ cache, uint8_t *__restrict__ ckpt,
                         (t_lo - j * g.block_size) * int64_t(tok);
     const int32_t nv = tb * vpt;  // vectors of the K (or V) run to copy
     for (int32_t l = l_first; l < l_end; ++l) {
-    const uint8_t *k_run = cache + int64_t(l * 2) * g.slab_bytes + blk;
-    const uint8_t *v_run = k_run + g.slab_bytes;
-    for (int32_t v0 = ta * vpt; v0 < nv; v0 += kWave * kUnroll) {
-      uint4 ka[kUnroll], va[kUnroll];
+      const uint8_t *k_run = cache + int64_t(l * 2) * g.slab_bytes + blk;
+      const uint8_t *v_run = k_run + g.slab_bytes;
+      for (int32_t v0 = ta * vpt; v0 < nv; v0 += kWave * kUnroll) {
+        uint4 ka[kUnroll], va[kUnroll];
 #pragma unroll
-      for (int k = 0; k < kUnroll; ++k) {
-        const int32_t v = v0 + k * kWave + lane;
-        ka[k] = make_uint4(0, 0, 0, 0);
-        va[k] = make_uint4(0, 0, 0, 0);
-        if (v < nv) {
-          ka[k] = load16<(nt_policy<true>() & 1) != 0>(k_run + int64_t(v) * 16);
-          va[k] = load16<(nt_policy<true>() & 1) != 0>(v_run + int64_t(v) * 16);
+        for (int k = 0; k < kUnroll; ++k) {
+          const int32_t v = v0 + k * kWave + lane;
+          ka[k] = make_uint4(0, 0, 0, 0);
+          va[k] = make_uint4(0, 0, 0, 0);
+          if (v < nv) {
+            ka[k] = load16<(nt_policy<true>() & 1) != 0>(k_run + int64_t(v) * 16);
+            va[k] = load16<(nt_policy<true>() & 1) != 0>(v_run + int64_t(v) * 16);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+          const int32_t v = v0 + k * kWave + lane;
+          if (v < nv) {
+            const uint32_t t = fdiv(uint32_t(v), g.div_kv);
+            const int64_t w = int64_t(v) - int64_t(t) * vpt;
+            uint8_t *q = ckpt + (row0 + t) * g.row_bytes +
+                         int64_t(l * 2) * tok + w * 16;
+            store16<(nt_policy<true>() & 2) != 0>(q, ka[k]);
+            store16<(nt_policy<true>() & 2) != 0>(q + tok, va[k]);
+          }
         }
       }
-#pragma unroll
-      for (int k = 0; k < kUnroll; ++k) {
-        const int32_t v = v0 + k * kWave + lane;
-        if (v < nv) {
-          const uint32_t t = fdiv(uint32_t(v), g.div_kv);
-          const int64_t w = int64_t(v) - int64_t(t) * vpt;
-          uint8_t *q = ckpt + (row0 + t) * g.row_bytes + int64_t(l * 2) * tok +
-                       w * 16;
-          store16<(nt_policy<true>() & 2) != 0>(q, ka[k]);
-          store16<(nt_policy<true>() & 2) != 0>(q + tok, va[k]);
-        }
-      }
-    }
     }
   }
 }
@@ -1282,6 +1298,7 @@ constexpr int32_t kNoAllocMaxReqs = LUMEN_KV_CKPT_NOALLOC_MAX_REQS;
 // The range walk keeps a prefix of 8 bytes per request in each
 // workgroup's LDS (32 KiB at the limit).
 constexpr int32_t kRangesMaxReqs = LUMEN_KV_CKPT_RANGES_MAX_REQS;
+constexpr int64_t kMaxUnits = LUMEN_KV_CKPT_MAX_UNITS;
 // The page-major pack over the ranges keeps two prefixes (tokens and
 // pages) in LDS; above this many requests the range path packs
 // token-major instead.
@@ -1514,6 +1531,7 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   g.unit_vecs = int32_t(2 * H * d_bytes / 16);
   g.bt_cols = bt_cols;
   g.num_reqs = num_reqs;
+  g.max_rows = kMaxUnits / lay->num_layers;
   g.div_unit = make_fastdiv(uint32_t(g.unit_vecs));
   g.div_kv = make_fastdiv(uint32_t(H * d_bytes / 16));
   g.div_head = make_fastdiv(uint32_t(d_bytes / 16));
@@ -1718,7 +1736,6 @@ int direct_copy(bool pack, const lumen_kv_layout *layout, const void *cache,
                             row_begin, row_end, ckpt_first_row, ckpt_rows,
                             stream, waves);
 }
-}  // namespace
 
 // Plan and copy in one launch over the ranges (the _ranges entry points).
 int ranges_copy(bool pack, const lumen_kv_layout *lay, void *cache,
@@ -1738,6 +1755,7 @@ int ranges_copy(bool pack, const lumen_kv_layout *lay, void *cache,
                      bt_cols, num_reqs, nullptr, 0, INT64_MAX, 0, ckpt_rows,
                      stream, 0, d_status, &ranges);
 }
+}  // namespace
 
 extern "C" {
 
@@ -2104,7 +2122,7 @@ const char *lumen_kv_ckpt_strerror(int code) {
              "exhausted";
     case LUMEN_ERR_DUP_BLOCK: return "block named by two pages of an unpack";
     case LUMEN_ERR_TOO_MANY:
-      return "more requests than the call takes in one launch";
+      return "more requests or token rows than the call takes in one launch";
     default: return "unknown status";
   }
 }

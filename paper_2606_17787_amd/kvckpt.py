@@ -38,6 +38,7 @@ LUMEN_ERR_DUP_BLOCK = -8
 LUMEN_ERR_TOO_MANY = -9
 LUMEN_KV_CKPT_NOALLOC_MAX_REQS = 16384  # include/lumen_kv_ckpt.h
 LUMEN_KV_CKPT_RANGES_MAX_REQS = 4096  # include/lumen_kv_ckpt.h
+LUMEN_KV_CKPT_MAX_UNITS = 1 << 40  # include/lumen_kv_ckpt.h
 LUMEN_CACHE_NHD = 0
 LUMEN_CACHE_HND = 1
 

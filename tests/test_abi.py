@@ -36,6 +36,48 @@ def test_exports_every_declared_entry_point(lib):
         assert hasattr(lib, n), n
 
 
+def _header_defines():
+    """Integer #defines of the header, evaluated: decimal literals,
+    parentheses, unary minus, an int64_t cast and a left shift."""
+    import ast
+    import os
+    import re
+    path = os.path.join(os.path.dirname(os.path.dirname(
+        os.path.abspath(__file__))), "include", "lumen_kv_ckpt.h")
+    out = {}
+    for m in re.finditer(r"^#define (LUMEN_\w+) +(\(.*?\)|-?\d+)(?: |$)",
+                         open(path).read(), re.M):
+        expr = m.group(2).replace("(int64_t)", "")
+        node = ast.parse(expr, mode="eval").body
+
+        def ev(n):
+            if isinstance(n, ast.Constant) and isinstance(n.value, int):
+                return n.value
+            if isinstance(n, ast.UnaryOp) and isinstance(n.op, ast.USub):
+                return -ev(n.operand)
+            if isinstance(n, ast.BinOp) and isinstance(n.op, ast.LShift):
+                return ev(n.left) << ev(n.right)
+            raise ValueError(f"{m.group(1)}: {expr}")
+        out[m.group(1)] = ev(node)
+    return out
+
+
+def test_binding_constants_match_the_header():
+    """Every status code, layout tag and limit the binding names has the
+    header's value."""
+    defines = _header_defines()
+    names = [n for n in dir(kv) if n.startswith("LUMEN_")
+             and isinstance(getattr(kv, n), int)]
+    assert len(names) >= 15
+    for n in names:
+        assert n in defines, n
+        assert getattr(kv, n) == defines[n], (n, getattr(kv, n), defines[n])
+    # and the binding knows every status code
+    codes = [n for n in defines if n.startswith("LUMEN_ERR_")]
+    assert len(codes) == 9 and all(hasattr(kv, n) for n in codes)
+    assert defines["LUMEN_KV_CKPT_MAX_UNITS"] == 2 ** 40
+
+
 def test_exports_every_page_tag_entry_point(lib):
     from paper_2606_17787_amd import tags
     names = tags.exported_names()

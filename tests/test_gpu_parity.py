@@ -365,6 +365,82 @@ def test_error_inputs_still_copy_every_valid_row(case, walk, via):
         f"{walk}: unpack wrote other slots than the valid tokens'"
 
 
+@pytest.mark.parametrize("walk", list(ERROR_WALK_SHAPES))
+@pytest.mark.parametrize("via", VIAS)
+def test_ranges_past_the_unit_limit_copy_nothing(walk, via):
+    """Ranges holding more (token row, layer) units than one launch walks
+    (LUMEN_KV_CKPT_MAX_UNITS): ends of INT32_MAX on 1,024 requests are
+    about 2^41 token rows.  Pack and unpack record TOO_MANY and write
+    nothing, at once instead of walking rows that are all invalid, on
+    every walk."""
+    shape = ERROR_WALK_SHAPES[walk]
+    R, nb, rows = 1024, 8, 16
+    s = np.zeros(R, np.int32)
+    e = np.full(R, 2**31 - 1, np.int32)
+    assert R * (2**31 - 1) * shape.num_layers > kv.LUMEN_KV_CKPT_MAX_UNITS
+    bt = (np.arange(R * 2, dtype=np.int32) % nb).reshape(R, 2)
+    rng = np.random.default_rng(77)
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    st, ck, got_dst = gpu_path(shape, nb, src, bt, s, e, nb, dst, bt,
+                               ckpt_rows=rows, via=via)
+    assert st == kv.LUMEN_ERR_TOO_MANY
+    assert (ck == SENTINEL).all()
+    assert np.array_equal(got_dst, dst)
+
+
+@pytest.mark.parametrize("walk", list(ERROR_WALK_SHAPES))
+@pytest.mark.parametrize("via", VIAS)
+def test_long_invalid_ranges_still_copy_their_valid_rows(walk, via):
+    """Ranges far past their block tables but inside the unit limit: a
+    range of 2^20 tokens whose first 12 lie in its table, and one ending at
+    INT32_MAX.  The walk crosses all their rows: the status is the
+    oracle's (RANGE), the 12 valid rows equal the oracle's pack of those
+    tokens, every other row keeps its sentinel, and the unpack writes those
+    tokens' slots only."""
+    shape = ERROR_WALK_SHAPES[walk]
+    nb, rows = 8, 64
+    s = np.array([0, 2**31 - 6], np.int32)
+    e = np.array([2**20, 2**31 - 1], np.int32)
+    bt = np.array([[0, 1, 2], [3, 4, 5]], np.int32)
+    n_ok = bt.shape[1] * shape.block_size  # request 0's tokens in its table
+    rng = np.random.default_rng(78)
+    src = W.random_bits(rng, shape.pool_elems(nb))
+    dst = W.random_bits(rng, shape.pool_elems(nb))
+    ck_in = W.random_bits(rng, rows * shape.token_row_elems).reshape(rows, -1)
+    st_o, _ = oracle.pack(shape, nb, src, bt, s, e, ckpt=np.zeros(
+        (rows, shape.token_row_elems), np.uint16), ckpt_rows=rows)
+    assert st_o == oracle.ERR_RANGE
+    want_ck = np.full((rows, shape.token_row_elems), SENTINEL, np.uint16)
+    st, want_ck[:n_ok] = oracle.pack(shape, nb, src, bt[:1], [0], [n_ok])
+    assert st == oracle.OK
+    want_dst = dst.copy()
+    assert oracle.unpack(shape, nb, want_dst, bt[:1], [0], [n_ok],
+                         ck_in[:n_ok]) == oracle.OK
+
+    d_s, d_e, d_bt = h2d(s), h2d(e), h2d(bt)
+    ck = h2d(np.full(rows * shape.token_row_elems, SENTINEL, np.uint16))
+    ws = kv.new_workspace(len(s), dev())
+
+    def copy(pack, cache, ckpt):
+        if via == "ranges":
+            status = torch.zeros(1, dtype=torch.int32, device=dev())
+            fn = (kv.lumen_kv_ckpt_pack_ranges if pack
+                  else kv.lumen_kv_ckpt_unpack_ranges)
+            fn(shape, nb, cache, d_bt, d_s, d_e, ckpt, status)
+            return int(status.item())
+        kv.lumen_kv_ckpt_plan(d_s, d_e, ws)
+        fn = kv.lumen_kv_ckpt_pack if pack else kv.lumen_kv_ckpt_unpack
+        fn(shape, nb, cache, d_bt, ws, ckpt)
+        return kv.lumen_kv_ckpt_status(ws)
+
+    assert copy(True, h2d(src), ck) == st_o
+    assert np.array_equal(d2h16(ck).reshape(rows, -1), want_ck)
+    d_dst = h2d(dst)
+    assert copy(False, d_dst, h2d(ck_in)) == st_o
+    assert np.array_equal(d2h16(d_dst), want_dst)
+
+
 def test_status_clears_the_error_word():
     shape = CacheShape(1, 1, 8, 4, NHD)
     nb = 2

@@ -319,6 +319,29 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     def events(n):
         return {i: [TimingEvent() for _ in range(4)] for i in n}
 
+    def self_check(last, bufs):
+        """The last timed step checked without an oracle, before a later
+        pass rewrites its buffers (the passes over one placement at a time
+        map steps to other regions): its pack's region equals a fresh pack
+        of its step, and re-packing the tokens its unpack restored gives
+        back the region that unpack read."""
+        (k1, k2), (dst, arena) = last, bufs
+        ok = True
+        for k, pool, nb, table in ((k1, src, w.num_blocks, bt),
+                                   (k2, dst, w.dst_num_blocks, bt_dst)):
+            n = int(rows[k])
+            out = torch.empty(n * row_elems, dtype=torch.bfloat16, device=dev)
+            kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_b, 0)
+            kv.lumen_kv_ckpt_pack(sh, nb, pool, table, ws_b, out)
+            r0 = int(region_row[k])
+            region = arena[r0 * row_elems:(r0 + n) * row_elems]
+            ok = ok and bool(torch.equal(out.view(torch.int16),
+                                         region.view(torch.int16)))
+            assert kv.lumen_kv_ckpt_status(ws_b) == 0
+        if not ok:
+            say(f"[bench] {w.name}: self-check of the last timed step FAILED")
+        return ok
+
     # The timed pass (the value): exactly `steps` steps with nothing but
     # the copies and their plans on the stream.
     for i in range(warmup):
@@ -335,6 +358,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     # the same schedule position, each launch bracketed by HIP events on its
     # stream.  The events cost a few us per step, so they stay out of the
     # timed pass.
+    roundtrip = self_check(done[-1], sets[(warmup + steps - 1) % P])
     sampled = _event_steps(steps)
     ev = events(sampled)
     done_ev = [step(warmup + i, ev[i]) for i in sampled]
@@ -383,22 +407,6 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                 unpack_us_median=up["us_median"],
                 pack_us_p10_p90=pk["us_p10_p90"],
                 unpack_us_p10_p90=up["us_p10_p90"], samples=pk["samples"]))
-
-    # Round trip as a self-check (no oracle here): re-pack the restored
-    # tokens of one step from the restore pool and compare with the region
-    # the unpack read.
-    i_last = warmup + steps - 1
-    k = done[-1][1]
-    dst, arena = sets[i_last % P]
-    kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_b, 0)
-    back = torch.empty(int(rows[k]) * row_elems, dtype=torch.bfloat16,
-                       device=dev)
-    kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, dst, bt_dst, ws_b, back)
-    r0 = int(region_row[k])
-    region = arena[r0 * row_elems:(r0 + int(rows[k])) * row_elems]
-    roundtrip = bool(torch.equal(back.view(torch.int16),
-                                 region.view(torch.int16)))
-    assert kv.lumen_kv_ckpt_status(ws_b) == 0
 
     # The per-request row mode: one checkpoint per request (Sec. 4.2), the
     # increments of request r appending to its own region of the first

@@ -35,6 +35,8 @@
  *   pack_to_host_direct / unpack_from_host_direct
  *           the gather writing, or the scatter reading, pinned host memory
  *           itself on a small grid: no staging ring and no copy engine
+ *   time_next_copy
+ *           the next copy kernel's own start and end, on two HIP events
  *   validate_targets
  *           validate mode of a restore (duplicate target blocks)
  *   draft_align
@@ -465,6 +467,20 @@ int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream);
 
 /* Static string for a status code. */
 const char *lumen_kv_ckpt_strerror(int code);
+
+/* Times the next copy kernel this host thread launches, for callers that
+ * want a kernel's own duration with no marker commands of theirs on the
+ * stream around it (benchmarks, profilers).  start_event and stop_event
+ * are hipEvent_t handles created with timing enabled (either may be NULL).
+ * The next gather or scatter kernel of this thread (of a pack, unpack,
+ * their _rows, _ranges, _noalloc and _direct forms, or the first chunk of
+ * a pipeline) is launched through hipExtLaunchKernel with these events:
+ * `start` takes the time that kernel starts and `stop` the time it ends,
+ * so hipEventElapsedTime(start, stop) is its duration.  Plan and scan
+ * kernels are not timed.  Calls that launch no copy kernel (empty or
+ * refused ones) leave the pair armed; the launch that uses it clears it.
+ * Passing two NULLs disarms it.  Returns LUMEN_OK. */
+int lumen_kv_ckpt_time_next_copy(void *start_event, void *stop_event);
 
 /* Device -> host copy of `bytes` from d_src to h_dst on stream `side`,
  * ordered after all work enqueued on `producer` so far, so the main stream

@@ -39,6 +39,7 @@
 // the wait for it; there, where units are long, each wavefront copies two
 // spans so that one scan serves both.
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -1410,6 +1411,11 @@ int current_device(DeviceInfo **info) {
 
 bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
+// Takes an error that an earlier runtime call of this thread left pending
+// (the caller's, say a failed event query), so that the check after this
+// call's launches reports their own outcome only.
+void clear_pending_error() { (void)hipGetLastError(); }
+
 int check_layout(const lumen_kv_layout *lay) {
   if (!lay) return LUMEN_ERR_INVALID_ARG;
   if (lay->num_layers <= 0 || lay->num_kv_heads <= 0 || lay->head_dim <= 0 ||
@@ -1445,34 +1451,55 @@ int check_copy_buffers(const lumen_kv_layout *lay, const void *cache,
   return LUMEN_OK;
 }
 
+// Events for the next copy kernel of this thread (lumen_kv_ckpt_time_next_copy).
+struct Timing {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+  bool armed = false;
+};
+thread_local Timing next_timing;
+
+Timing take_timing() {
+  const Timing t = next_timing;
+  next_timing = Timing{};
+  return t;
+}
+
+// A kernel launch that carries the timing events when they are armed
+// (hipExtLaunchKernel stamps the kernel's own start and end on them).
+#define LUMEN_LAUNCH(tm, kernel, grid, block, lds, s, ...)                    \
+  do {                                                                       \
+    if ((tm).armed)                                                          \
+      hipExtLaunchKernelGGL(kernel, grid, block, uint32_t(lds), s,           \
+                            (tm).start, (tm).stop, 0, __VA_ARGS__);          \
+    else                                                                     \
+      hipLaunchKernelGGL(kernel, grid, block, lds, s, __VA_ARGS__);          \
+  } while (0)
+
 // max_waves > 0 caps the grid (a copy whose checkpoint side is host memory
 // across the host link needs a few hundred wavefronts, not the HBM grid) and
 // keeps the token-major walk, whose checkpoint accesses are sequential.
 template <class Walk>
 void launch_rows(bool pack, bool hnd, unsigned blocks, size_t lds,
-                 hipStream_t s, const uint8_t *in, uint8_t *out,
-                 const int32_t *bt, const void *p0, const void *p1,
-                 const void *p2, const void *p3, int64_t row_base,
-                 int32_t *err, const Geom &g) {
+                 hipStream_t s, const Timing &tm, const uint8_t *in,
+                 uint8_t *out, const int32_t *bt, const void *p0,
+                 const void *p1, const void *p2, const void *p3,
+                 int64_t row_base, int32_t *err, const Geom &g) {
   const dim3 grid(blocks), block(kBlockThreads);
   if (pack) {
     if (hnd)
-      hipLaunchKernelGGL((copy_rows_kernel<true, true, Walk>), grid, block,
-                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
-                         g);
+      LUMEN_LAUNCH(tm, (copy_rows_kernel<true, true, Walk>), grid, block, lds,
+                   s, in, out, bt, p0, p1, p2, p3, row_base, err, g);
     else
-      hipLaunchKernelGGL((copy_rows_kernel<true, false, Walk>), grid, block,
-                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
-                         g);
+      LUMEN_LAUNCH(tm, (copy_rows_kernel<true, false, Walk>), grid, block,
+                   lds, s, in, out, bt, p0, p1, p2, p3, row_base, err, g);
   } else {
     if (hnd)
-      hipLaunchKernelGGL((copy_rows_kernel<false, true, Walk>), grid, block,
-                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
-                         g);
+      LUMEN_LAUNCH(tm, (copy_rows_kernel<false, true, Walk>), grid, block,
+                   lds, s, in, out, bt, p0, p1, p2, p3, row_base, err, g);
     else
-      hipLaunchKernelGGL((copy_rows_kernel<false, false, Walk>), grid, block,
-                         lds, s, in, out, bt, p0, p1, p2, p3, row_base, err,
-                         g);
+      LUMEN_LAUNCH(tm, (copy_rows_kernel<false, false, Walk>), grid, block,
+                   lds, s, in, out, bt, p0, p1, p2, p3, row_base, err, g);
   }
 }
 
@@ -1576,6 +1603,8 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const uint8_t *in = static_cast<const uint8_t *>(src);
   uint8_t *out = static_cast<uint8_t *>(dst);
+  const Timing tm = take_timing();  // a copy kernel is launched below
+  clear_pending_error();
   const bool page_major = pack && !hnd && row_lo == 0 &&
                           row_hi == INT64_MAX && win_first == 0 &&
                           max_waves == 0 && use_page_major(H * d_bytes);
@@ -1584,25 +1613,25 @@ int launch_copy(bool pack, const lumen_kv_layout *lay, const void *src,
     // totals of both.
     const size_t lds =
         sizeof(int64_t) * (2 * (size_t(num_reqs) + 1) + 2 * kWavesPerBlock);
-    hipLaunchKernelGGL((pack_pages_kernel<RangePages>), dim3(blocks),
-                       dim3(kBlockThreads), lds, s, in, out, bt,
-                       ranges->start, ranges->end, ranges->req_row_base,
-                       nullptr, nullptr, ranges->row_base, err, g);
+    LUMEN_LAUNCH(tm, (pack_pages_kernel<RangePages>), dim3(blocks),
+                 dim3(kBlockThreads), lds, s, in, out, bt, ranges->start,
+                 ranges->end, ranges->req_row_base, nullptr, nullptr,
+                 ranges->row_base, err, g);
   } else if (ranges) {
     // LDS: prefix[R + 1] and the wavefronts' totals.
     const size_t lds = sizeof(int64_t) * (size_t(num_reqs) + 1 + kWavesPerBlock);
-    launch_rows<RangeWalk>(pack, hnd, row_blocks, lds, s, in, out, bt,
+    launch_rows<RangeWalk>(pack, hnd, row_blocks, lds, s, tm, in, out, bt,
                            ranges->start, ranges->end, ranges->req_row_base,
                            nullptr, ranges->row_base, err, g);
   } else if (page_major) {
     hipLaunchKernelGGL(item_scan_kernel, dim3(1), dim3(kPlanThreads), 0, s,
                        v.hdr, v.prefix, v.start, v.items, num_reqs,
                        lay->block_size);
-    hipLaunchKernelGGL((pack_pages_kernel<WsPages>), dim3(blocks),
-                       dim3(kBlockThreads), 0, s, in, out, bt, v.hdr,
-                       v.prefix, v.first_row, v.start, v.items, 0, err, g);
+    LUMEN_LAUNCH(tm, (pack_pages_kernel<WsPages>), dim3(blocks),
+                 dim3(kBlockThreads), 0, s, in, out, bt, v.hdr, v.prefix,
+                 v.first_row, v.start, v.items, 0, err, g);
   } else {
-    launch_rows<WsWalk>(pack, hnd, row_blocks, 0, s, in, out, bt, v.hdr,
+    launch_rows<WsWalk>(pack, hnd, row_blocks, 0, s, tm, in, out, bt, v.hdr,
                         v.prefix, v.first_row, v.start, 0, err, g);
   }
   return hipGetLastError() == hipSuccess ? LUMEN_OK : LUMEN_ERR_HIP;
@@ -1774,6 +1803,7 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
   int st = current_device(&dev);
   if (st != LUMEN_OK) return st;
   WsView v = ws_view(d_workspace, num_reqs);
+  clear_pending_error();
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0,
                      static_cast<hipStream_t>(stream), d_start, d_end,
                      num_reqs, row_base, d_req_row_base, v.hdr, v.prefix,
@@ -1820,6 +1850,7 @@ int lumen_kv_ckpt_pack_noalloc(const lumen_kv_layout *layout,
   // header and per-request arrays) and the status word, so nothing left by
   // an earlier call is seen.
   WsView v = ws_view(dev->scratch, num_reqs);
+  clear_pending_error();
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0,
                      static_cast<hipStream_t>(stream), d_start, d_end,
                      num_reqs, row_base, d_req_row_base, v.hdr, v.prefix,
@@ -1915,6 +1946,7 @@ int lumen_kv_ckpt_validate_targets(const lumen_kv_layout *layout,
   WsView v = ws_view(d_workspace, num_reqs);
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int64_t n16 = int64_t(need / 16);
+  clear_pending_error();
   if (n16 > 0) {
     const int64_t cap = int64_t(dev->cus) * 4;
     int64_t blocks = (n16 + kBlockThreads - 1) / kBlockThreads;
@@ -2075,6 +2107,7 @@ int lumen_kv_draft_align(const int32_t *d_draft, int32_t draft_cols,
   if (st != LUMEN_OK) return st;
   WsView v = ws_view(d_workspace, num_reqs);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  clear_pending_error();
   if (num_reqs > 0) {
     int64_t blocks = (int64_t(num_reqs) + kWavesPerBlock - 1) / kWavesPerBlock;
     const int64_t cap = int64_t(dev->cus) * 8;
@@ -2106,6 +2139,13 @@ int lumen_kv_ckpt_status(void *d_workspace, lumen_stream_t stream) {
     return LUMEN_ERR_HIP;
   if (hipStreamSynchronize(s) != hipSuccess) return LUMEN_ERR_HIP;
   return code;
+}
+
+int lumen_kv_ckpt_time_next_copy(void *start_event, void *stop_event) {
+  next_timing.start = static_cast<hipEvent_t>(start_event);
+  next_timing.stop = static_cast<hipEvent_t>(stop_event);
+  next_timing.armed = start_event || stop_event;
+  return LUMEN_OK;
 }
 
 const char *lumen_kv_ckpt_strerror(int code) {

@@ -123,6 +123,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "lumen_kv_ckpt_validate_targets": (ctypes.c_int,
                                            [lay, p, i32, i32, p, p, sz, p]),
         "lumen_kv_ckpt_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "lumen_kv_ckpt_time_next_copy": (ctypes.c_int, [p, p]),
         "lumen_kv_ckpt_offload": (ctypes.c_int, [p, p, sz, p, p]),
         "lumen_kv_ckpt_stage_in": (ctypes.c_int, [p, p, sz, p, p]),
     }
@@ -215,6 +216,21 @@ def lumen_kv_ckpt_plan_workspace_bytes(num_reqs: int) -> int:
 
 def lumen_kv_ckpt_strerror(code: int) -> str:
     return load_library().lumen_kv_ckpt_strerror(code).decode()
+
+
+def lumen_kv_ckpt_time_next_copy(start_event, stop_event) -> None:
+    """Time the next copy kernel this thread launches on two HIP events
+    (raw hipEvent_t handles as ints or ctypes pointers, created with timing
+    enabled; None for either): `start` takes the time that kernel starts,
+    `stop` the time it ends.  Calls that launch no copy kernel leave them
+    armed; the launch that uses them clears them."""
+    def raw(ev):
+        if ev is None:
+            return None
+        return ev.value if isinstance(ev, ctypes.c_void_p) else int(ev)
+    _check(load_library().lumen_kv_ckpt_time_next_copy(raw(start_event),
+                                                       raw(stop_event)),
+           "lumen_kv_ckpt_time_next_copy")
 
 
 def new_workspace(num_reqs: int, device=None) -> torch.Tensor:

@@ -413,18 +413,19 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                 unpack_us_p10_p90=up["us_p10_p90"], samples=pk["samples"]))
 
     # The per-request row mode: one checkpoint per request (Sec. 4.2), the
-    # increments of request r appending to its own region of the first
-    # arena, so a step's rows land in up to R places instead of one run.
-    # Steps 0 .. NR-1 fill the arena exactly.
-    dst, arena = sets[0]
+    # increments of request r appending to its own region of the arena, so a
+    # step's rows land in up to R places instead of one run.  Steps
+    # 0 .. NR-1 fill an arena exactly; the steps rotate over the placements
+    # as in the timed pass.
     inc = w.ends[NR - 1].astype(np.int64) - w.starts[0].astype(np.int64)
     assert int(inc.sum()) == int(rows[:NR].sum()) <= arena_rows
     region0 = np.concatenate([[0], np.cumsum(inc)[:-1]])
     rrb_h = region0 - w.starts[0].astype(np.int64)  # row of token t: rrb + t
     rrb = torch.from_numpy(rrb_h).to(dev)
-    for k in range(NR):
-        kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
-        kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
+    for _, arena in sets:
+        for k in range(NR):
+            kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0, rrb)
+            kv.lumen_kv_ckpt_pack(sh, w.num_blocks, src, bt, ws_a, arena)
     assert kv.lumen_kv_ckpt_status(ws_a) == 0
     pr_steps = max(steps // 2, MIN_KERNEL_SAMPLES)
 
@@ -433,6 +434,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     def step_pr(i, events=None):
         k = i % NR
         k2 = (k + lag) % NR
+        dst, arena = sets[i % P]
         copies(pr_path, k, k2, dst, arena, events, rrb)
         return k, k2
 
@@ -451,8 +453,10 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
     pr_pack, pr_unpack = sampled_stats(pr_done_ev, pr_ev, pr_sampled)
     pr_step_b = sum(2.0 * (rows[k] + rows[k2]) * rb for k, k2 in pr_done)
     # self-check: one step's rows, gathered from the request regions, equal
-    # the same step packed contiguously
+    # the same step packed contiguously (every arena holds every step's
+    # rows in its regions)
     k = pr_done[-1][0]
+    arena = sets[(warmup + pr_steps - 1) % P][1]
     kv.lumen_kv_ckpt_plan(starts[k], ends[k], ws_a, 0)
     back = torch.empty(int(rows[k]) * row_elems, dtype=torch.bfloat16,
                        device=dev)
@@ -466,7 +470,8 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
                              back.view(torch.int16)))
     assert kv.lumen_kv_ckpt_status(ws_a) == 0
     per_request_mode = dict(
-        path=pr_path, steps=pr_steps, ms_per_step=(t3 - t2) * 1e3 / pr_steps,
+        path=pr_path, steps=pr_steps, placements=P,
+        ms_per_step=(t3 - t2) * 1e3 / pr_steps,
         step_GBps=gb(pr_step_b) / (t3 - t2),
         pack_GBps=pr_pack["GBps"], unpack_GBps=pr_unpack["GBps"],
         pack_us_median=pr_pack["us_median"],
@@ -474,7 +479,7 @@ def incremental_leg(torch, kv, w, steps, warmup, seed, keep=None,
         samples=pr_pack["samples"], check_ok=pr_ok)
     if keep is not None:
         keep["sizes"], keep["bufs"] = sizes, (src, sets[0][0], sets[0][1])
-    del src, sets, dst, arena, back, gathered
+    del src, sets, arena, back, gathered
     if keep is None:
         torch.cuda.empty_cache()
 

@@ -99,3 +99,47 @@ def test_events_wait_for_a_launch_and_serve_one():
     torch.cuda.synchronize()
     assert a.elapsed_time(b) == first
     assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK
+
+
+def _leave_a_pending_error():
+    """A failed runtime query of the caller's (elapsed time of events never
+    recorded) leaves an error pending in this thread."""
+    a, b = bench.TimingEvent(), bench.TimingEvent()
+    with pytest.raises(RuntimeError):
+        a.elapsed_time(b)
+
+
+def test_calls_report_their_own_launches_after_a_pending_error():
+    """Plan, pack, the one-launch copy and validate mode each report the
+    outcome of their own launches, not an error an earlier, unrelated
+    runtime call left pending."""
+    shape = CacheShape(2, 2, 64, 4, NHD)
+    rng = np.random.default_rng(93)
+    nb = 8
+    bt = np.array([[0, 1, 2], [3, 4, 5]], np.int32)
+    s, e = np.array([0, 2], np.int32), np.array([12, 9], np.int32)
+    rows = int((e - s).sum())
+    src_h = W.random_bits(rng, shape.pool_elems(nb))
+    src = h2d(src_h)
+    d_s, d_e, d_bt = h2d(s), h2d(e), h2d(bt)
+    ck = torch.zeros(rows * shape.token_row_elems, dtype=torch.int16,
+                     device=dev())
+    ws = kv.new_workspace(2, dev())
+    _leave_a_pending_error()
+    kv.lumen_kv_ckpt_plan(d_s, d_e, ws)
+    _leave_a_pending_error()
+    kv.lumen_kv_ckpt_pack(shape, nb, src, d_bt, ws, ck)
+    _leave_a_pending_error()
+    kv.lumen_kv_ckpt_validate_targets(shape, nb, d_bt, ws,
+                                      kv.new_marks(nb, dev()))
+    assert kv.lumen_kv_ckpt_status(ws) == kv.LUMEN_OK
+    status = torch.zeros(1, dtype=torch.int32, device=dev())
+    ck2 = torch.zeros_like(ck)
+    _leave_a_pending_error()
+    kv.lumen_kv_ckpt_pack_ranges(shape, nb, src, d_bt, d_s, d_e, ck2, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == kv.LUMEN_OK
+    st, want = oracle.pack(shape, nb, src_h, bt, s, e)
+    assert st == oracle.OK
+    for got in (ck, ck2):
+        assert np.array_equal(d2h16(got).reshape(rows, -1), want)

@@ -1179,9 +1179,10 @@ def tiny_leg(torch, kv, W, reps=200):
     from HIP events around each pair with the stream drained in between,
     the same pairs back to back, and the host cost of enqueueing one call
     through the binding, also with the calls prepared once (PreparedCall),
-    and the one-launch range copies prepared the same way.  Self-check:
+    and the one-launch range copies prepared the same way, alone and as a
+    round trip, issued eagerly or replayed from a HIP graph.  Self-check:
     the restored tokens, packed again from the destination pool, equal the
-    checkpoint."""
+    checkpoint (also after one graph replay)."""
     dev = torch.device("cuda:0")
     w = W.c1_tiny()
     sh = w.shape
@@ -1242,6 +1243,32 @@ def tiny_leg(torch, kv, W, reps=200):
     p_runpack = kv.prepare_unpack_ranges(sh, w.dst_num_blocks, dst, bt2, s,
                                          e, ck, status)
     pk_r, up_r = pair_us(p_rpack), pair_us(p_runpack)
+
+    # the round trip (pack, then unpack, one launch each) eagerly, and
+    # captured once in a HIP graph and replayed: one host call per trip
+    def roundtrip_ranges():
+        p_rpack()
+        p_runpack()
+
+    rt_eager = pair_us(roundtrip_ranges)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        roundtrip_ranges()
+    torch.cuda.synchronize()
+    rt_graph = pair_us(graph.replay)
+    # the replay's own result: a cleared checkpoint and pool, one replay,
+    # then the restored tokens packed again must equal the checkpoint
+    ck.zero_()
+    dst.zero_()
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    kv.lumen_kv_ckpt_plan(s, e, ws)
+    kv.lumen_kv_ckpt_pack(sh, w.dst_num_blocks, dst, bt2, ws, back)
+    graph_ok = bool(torch.equal(back, ck)) and bool(ck.any())
+    assert kv.lumen_kv_ckpt_status(ws) == 0
+    del graph
     if int(status.item()) != 0:
         raise RuntimeError("range copies reported "
                            f"{kv.lumen_kv_ckpt_strerror(int(status.item()))}")
@@ -1286,6 +1313,9 @@ def tiny_leg(torch, kv, W, reps=200):
             "prepared_host_enqueue_us_per_call": host_p_us,
             "prepared_ranges_pack_us_median": float(np.median(pk_r)),
             "prepared_ranges_unpack_us_median": float(np.median(up_r)),
+            "ranges_roundtrip_us_median": float(np.median(rt_eager)),
+            "graph_ranges_roundtrip_us_median": float(np.median(rt_graph)),
+            "graph_roundtrip_ok": graph_ok,
             "roundtrip_ok": ok}
 
 

@@ -66,8 +66,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
 METRIC = ("KV checkpoint pack/unpack GB/s and % of HBM peak, 1×MI355X; "
           "restore ms/request")
-ALL_LEGS = ("decode", "tiny", "qwen", "restore", "tp8", "stage", "tags",
-            "sched", "draft", "cpu")
+ALL_LEGS = ("decode", "tiny", "small", "qwen", "restore", "tp8", "stage",
+            "tags", "sched", "draft", "cpu")
 MIN_KERNEL_SAMPLES = 20  # fewest timed launches of a per-kernel figure
 
 
@@ -1172,6 +1172,102 @@ def draft_leg(torch, kv, reps=50):
             "freed_blocks": int(cnt.item()), "check_ok": ok}
 
 
+def small_steps_leg(torch, kv, W, sizes=(8, 32, 64, 128), steps=20):
+    """Decode steps of the first R requests of the Llama-3-8B-shaped
+    workload (R = 8 .. 128), as one-launch range copies.  A copy's grid is
+    sized by its checkpoint buffer's rows, so each step runs twice: into a
+    buffer of exactly its rows (what a caller that knows its step's token
+    count passes), and into the whole 20-region arena at the region's row
+    (as the headline loop does).  Median us per pack and unpack from
+    stamped events; the two placements of each step's rows are checked to
+    hold the same bytes."""
+    dev = torch.device("cuda:0")
+    w = W.c2_llama8b()
+    sh = w.shape
+    NR, lag = 20, 10
+    re_ = sh.token_row_elems
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    src = torch.empty(sh.pool_elems(w.num_blocks), dtype=torch.bfloat16,
+                      device=dev)
+    src.normal_(generator=g)
+    dst = torch.zeros(sh.pool_elems(w.dst_num_blocks), dtype=torch.bfloat16,
+                      device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    out = {}
+    for R in sizes:
+        st = [torch.from_numpy(np.ascontiguousarray(a[:R])).to(dev)
+              for a in w.starts[:NR]]
+        en = [torch.from_numpy(np.ascontiguousarray(a[:R])).to(dev)
+              for a in w.ends[:NR]]
+        bt = torch.from_numpy(np.ascontiguousarray(w.block_tables[:R])).to(dev)
+        bt2 = torch.from_numpy(
+            np.ascontiguousarray(w.dst_block_tables[:R])).to(dev)
+        rows = [int((w.ends[k][:R].astype(np.int64) - w.starts[k][:R]).sum())
+                for k in range(NR)]
+        stride = max(rows)
+        arena = torch.empty(NR * stride * re_, dtype=torch.bfloat16,
+                            device=dev)
+        for k in range(NR):
+            kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, st[k],
+                                         en[k], arena, status, k * stride)
+
+        def region(k):
+            return arena[k * stride * re_:(k * stride + rows[k]) * re_]
+
+        def step(i, tight, ev):
+            k, k2 = i % NR, (i + lag) % NR
+            stamp(ev[0], ev[1])
+            if tight:
+                kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, st[k],
+                                             en[k], region(k), status)
+            else:
+                kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, st[k],
+                                             en[k], arena, status, k * stride)
+            stamp(ev[2], ev[3])
+            if tight:
+                kv.lumen_kv_ckpt_unpack_ranges(sh, w.dst_num_blocks, dst, bt2,
+                                               st[k2], en[k2], region(k2),
+                                               status)
+            else:
+                kv.lumen_kv_ckpt_unpack_ranges(sh, w.dst_num_blocks, dst, bt2,
+                                               st[k2], en[k2], arena, status,
+                                               k2 * stride)
+            return k, k2
+
+        res = {}
+        for tight in (True, False):
+            for i in range(4):
+                step(i, tight, [TimingEvent() for _ in range(4)])
+            evs = [[TimingEvent() for _ in range(4)] for _ in range(steps)]
+            done = [step(i, tight, evs[i]) for i in range(steps)]
+            torch.cuda.synchronize()
+            pk = [e[0].elapsed_time(e[1]) * 1e3 for e in evs]
+            up = [e[2].elapsed_time(e[3]) * 1e3 for e in evs]
+            byts = 2.0 * np.mean([rows[k] for k, _ in done]) * sh.token_row_bytes
+            res["buffer_of_step_rows" if tight else "whole_arena"] = dict(
+                pack_us_median=float(np.median(pk)),
+                unpack_us_median=float(np.median(up)),
+                pack_GBps=gb(byts) / (float(np.median(pk)) / 1e6))
+        if int(status.item()) != 0:
+            raise RuntimeError("small steps reported "
+                               f"{kv.lumen_kv_ckpt_strerror(int(status.item()))}")
+        # both buffers receive the same rows: pack step 0 both ways
+        kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, st[0], en[0],
+                                     arena, status, 0)
+        a = region(0).clone()
+        region(0).zero_()
+        kv.lumen_kv_ckpt_pack_ranges(sh, w.num_blocks, src, bt, st[0], en[0],
+                                     region(0), status)
+        res["same_rows"] = bool(torch.equal(a.view(torch.int16),
+                                            region(0).view(torch.int16)))
+        res["rows_per_step_mean"] = float(np.mean(rows))
+        out[str(R)] = res
+        del arena, a
+    torch.cuda.empty_cache()
+    return out
+
+
 def tiny_leg(torch, kv, W, reps=200):
     """The tiny full-pack workload (2 layers, 2 KV heads, head_dim 64,
     block 16; 8 requests, 1,729 tokens, 1.77 MB each way) is launch-bound,
@@ -1573,6 +1669,10 @@ def main():
     if "tiny" in legs:
         say("[bench] tiny leg (latency)")
         out["workloads"]["tiny"] = rounded(tiny_leg(torch, kv, W))
+    if "small" in legs:
+        say("[bench] small decode steps leg")
+        out["workloads"]["small-decode-steps"] = rounded(
+            small_steps_leg(torch, kv, W))
     if "qwen" in legs:
         say("[bench] decode leg (qwen-gqa-hnd)")
         q = W.c5_qwen_hnd()

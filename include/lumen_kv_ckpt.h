@@ -182,7 +182,7 @@ int lumen_kv_ckpt_plan(const int32_t *d_start, const int32_t *d_end,
  * buffer or window sized to the plan's rows keeps small steps free of idle
  * wavefronts: the pack of an 8-request Llama-3-8B-shaped decode step (65
  * rows) takes 8.4 us into a buffer of its rows and 20-31 us into a
- * multi-step arena, whose size sets the grid. */
+ * multi-step arena, whose size sets the grid.
  *
  * Walk.  A pack of a token-major cache whose token runs (H*D*elem_bytes
  * bytes per layer and K/V) are at most 512 bytes is done page by page: whole

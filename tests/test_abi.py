@@ -379,3 +379,23 @@ def test_draft_align_host_validation(lib):
     assert call(kl=None) == kv.LUMEN_ERR_INVALID_ARG
     assert call(freed=None) == kv.LUMEN_ERR_INVALID_ARG
     assert call(ws=FAKE_ODD) == kv.LUMEN_ERR_MISALIGNED
+
+
+@pytest.mark.parametrize("header", ["lumen_kv_ckpt.h", "lumen_page_tags.h",
+                                    "lumen_sched.h", "lumen_progress.h"])
+@pytest.mark.parametrize("lang", ["c", "c++"])
+def test_headers_compile_on_their_own(header, lang):
+    """Each public header parses alone as C and as C++ (no HIP headers
+    needed), with warnings as errors."""
+    import os
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc" if lang == "c" else "g++")
+    if cc is None:
+        pytest.skip("no host compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    inc = os.path.join(root, "include")
+    r = subprocess.run([cc, "-x", lang, "-fsyntax-only", "-Wall", "-Werror",
+                        "-I", inc, os.path.join(inc, header)],
+                       capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr

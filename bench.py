@@ -28,6 +28,9 @@ its start and end, on its stream (lumen_kv_ckpt_time_next_copy).
 Further legs (reported beside the headline, not part of its value):
   * tiny            the 8-request, 1.77 MB full pack and restore: launch
                     latency, back-to-back rate and host enqueue cost
+  * small           decode steps of the first 8 .. 128 requests, into a
+                    buffer of the step's rows and into a multi-step arena
+                    (the grid follows the checkpoint buffer)
   * qwen-gqa-hnd    the same decode loop on the head-major Qwen-style cache
   * qwen-gqa-nhd-twin  the same requests and tables over a token-major cache,
                     on the same buffers (what the head-major transpose costs)
